@@ -1,0 +1,126 @@
+"""Independent brute-force formulations used to pin the oracle (tiny inputs only).
+
+Nothing here calls the oracle; each function is a different formulation of a step of the
+method (arXiv 2605.06554), written so that a mistake in the oracle's version would show.
+"""
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+import numpy as np
+
+
+def level_offsets(N, p, L):
+    offs, o = [], 0
+    for l in range(L):
+        offs.append(o)
+        o += N // p ** l
+    return offs, o
+
+
+def pool_exact(x, p, l):
+    """Eq. pool with exact rational arithmetic: list of level-l rows (Fractions)."""
+    w = p ** l
+    N, D = len(x), len(x[0])
+    return [[sum(Fraction(float(x[i * w + t][c])) for t in range(w)) / w for c in range(D)]
+            for i in range(N // w)]
+
+
+def round_bf16_exact(x: Fraction) -> float:
+    """Nearest bf16 value to an exact rational, ties to even (8 significant bits)."""
+    if x == 0:
+        return 0.0
+    ax = abs(x)
+    m, e = math.frexp(float(ax))           # float(ax) ~ ax; fix the binade exactly below
+    while Fraction(2) ** (e - 1) > ax:
+        e -= 1
+    while Fraction(2) ** e <= ax:
+        e += 1
+    ulp = Fraction(2) ** (e - 8)            # ax in [2^(e-1), 2^e): 8 significant bits
+    r = round(ax / ulp) * ulp               # round() on a Fraction is half-to-even
+    return float(r if x > 0 else -r)
+
+
+def norms_fsum(x):
+    """Eq. score-base with an exactly rounded sum (math.fsum) and sqrt, rounded to fp32."""
+    return np.array([np.float32(math.sqrt(math.fsum(float(v) * float(v) for v in row))) for row in x],
+                    np.float32)
+
+
+def maxpool_levels(s0, p, L):
+    """Eq. score-pool by reshaping: level l = max over windows of p^l level-0 scores."""
+    s0 = np.asarray(s0, np.float32)
+    return [s0.reshape(-1, p ** l).max(axis=1) for l in range(L)]
+
+
+def select_stream(sqk_levels, skq_levels, p, L, k, replace_parents=False):
+    """Per-level descent where each level's parents are found by walking the CONCATENATED
+    QK and KQ streams (Eq. topk) in (score desc, index asc) order and keeping the first k
+    distinct entries. Returns the emitted level-local index sets, one sorted list per level."""
+    cand = list(range(len(sqk_levels[L - 1])))
+    emitted = [None] * L
+    for l in range(L - 1, -1, -1):
+        if l == 0:
+            emitted[0] = sorted(cand)
+            break
+        stream = [(float(sqk_levels[l][i]), i) for i in cand] + [(float(skq_levels[l][i]), i) for i in cand]
+        stream.sort(key=lambda t: (-t[0], t[1]))
+        parents, seen = [], set()
+        for _, i in stream:
+            if len(parents) >= k:
+                break
+            if i not in seen:
+                seen.add(i)
+                parents.append(i)
+        emitted[l] = sorted(set(cand) - set(parents)) if replace_parents else sorted(cand)
+        cand = sorted(p * i + r for i in parents for r in range(p))
+    return emitted
+
+
+def causal_sorted(emitted, N, p, L):
+    """Causal order of Sec. 3.5: (window end asc, coarser level first). Returns [(l, i)]."""
+    ent = [(l, i) for l in range(L) for i in emitted[l]]
+    ent.sort(key=lambda e: ((e[1] + 1) * p ** e[0] - 1, -e[0]))
+    return ent
+
+
+def causal_sdpa(q, k, v, scale):
+    """Plain causal softmax attention over rows, fp64 (Eq. sdpa)."""
+    S = len(q)
+    a = (q @ k.T) * scale
+    a = np.where(np.tril(np.ones((S, S), bool)), a, -np.inf)
+    a = a - a.max(axis=1, keepdims=True)
+    w = np.exp(a)
+    w /= w.sum(axis=1, keepdims=True)
+    return w @ v
+
+
+def all_pyramid_attention(q, k, v, p, L, scale):
+    """Cumulative selection with a budget covering every entry emits the whole pyramid. This
+    computes that layer with no sort and no index bookkeeping: a double loop over all pyramid
+    entries with the visibility predicate end(t) < end(m), or equal ends and level(t) >= level(m),
+    then the shifted range sums of Eq. fanout/scatter written as explicit loops.
+    q, k, v: [N, D] fp64 (pooled entries are NOT rounded). Returns O [N, D]."""
+    N, D = q.shape
+    ent = []  # (level, i, end, pooled q, k, v)
+    for l in range(L):
+        w = p ** l
+        for i in range(N // w):
+            sl = slice(i * w, (i + 1) * w)
+            ent.append((l, i, (i + 1) * w - 1, q[sl].mean(0), k[sl].mean(0), v[sl].mean(0)))
+    O = np.zeros((N, D))
+    for (lm, im, em, qm, _, _) in ent:
+        logits, vals = [], []
+        for (lt, it, et, _, kt, vt) in ent:
+            if et < em or (et == em and lt >= lm):
+                logits.append(scale * float(qm @ kt))
+                vals.append(vt)
+        logits = np.array(logits)
+        wts = np.exp(logits - logits.max())
+        om = (wts[:, None] * np.array(vals)).sum(0) / wts.sum()
+        w = p ** lm
+        for j in range(em, em + w):
+            if j < N:
+                O[j] += om
+    return O
