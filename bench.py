@@ -1,0 +1,274 @@
+"""Benchmark: Lighthouse attention forward + backward on one MI355X.
+
+One step = lh_attention_fwd + lh_attention_bwd on one batch of synthetic input that is
+already resident in HBM: pool, score, select, gather, SDPA, scatter, then the scatter adjoint,
+the SDPA backward, and the gather and pool adjoints. The workload is GQA with 32 query heads
+and 8 KV heads, N = 262144, D = 128, bf16, p = 4, L = 5, k = 4096 (S = 54272).
+
+The script prints one JSON line. `value` is tokens/s = B * N / step time. The timed region
+brackets exactly `--steps` steps with synchronisations. After it, each stage runs alone through
+its own C-ABI entry point, bracketed by HIP events on the stream the kernels run on. These give
+per-stage times and the roofline of the dominant stage. `cpu_baseline` times the fp64 oracle on a
+bounded sample of the same workload and extrapolates it by work counts.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def stage_work(pr, S, Ptot, es):
+    """Algorithmic bytes / flops per call of every stage (stage boundaries materialised)."""
+    B, N, Hq, Hkv, D = pr.B, pr.N, pr.Hq, pr.Hkv, pr.D
+    R = Ptot - N
+    BH = B * Hq
+    sdpa_pairs = B * Hq * S * (S + 1) / 2  # causal (query, key) pairs
+    return {
+        # read Q, K, V once; write levels 1..L-1 and the fp32 scores
+        "pool_score": ("hbm", (Hq + 2 * Hkv) * B * N * D * es + (Hq + 2 * Hkv) * B * R * D * es
+                       + (Hq + Hkv) * B * Ptot * 4),
+        # read both score streams of the candidates, write idx and the slot map
+        "select": ("hbm", BH * (2 * 4 * (S + 0) + 4 * S + 4 * Ptot)),
+        # read S rows of Q, K, V (pyramid or input) and write them
+        "gather": ("hbm", 6 * BH * S * D * es),
+        "sdpa_fwd": ("mfma", 4 * sdpa_pairs * D),
+        # read S rows of Otilde, write N rows of O
+        "scatter": ("hbm", BH * (S + N) * D * es),
+        # read N rows of dO, write S rows of dOtilde
+        "scatter_bwd": ("hbm", BH * (S + N) * D * es),
+        # dV = P^T dO, dP = dO V^T, dK = dS^T Q, dQ = dS K
+        "sdpa_bwd": ("mfma", 8 * sdpa_pairs * D),
+        # read S rows of dQ~, dK~, dV~; write dQ, dK, dV
+        "gather_bwd": ("hbm", 3 * BH * S * D * es + B * (Hq + 2 * Hkv) * N * D * es),
+    }
+
+
+def run_gpu(args, cfg):
+    import paper_2605_06554_amd as lh
+
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    inp = workloads.make_inputs(cfg, device=dev)
+    q, k, v, dout = inp["q"], inp["k"], inp["v"], inp["dout"]
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    pr = lh.problem(B, N, Hq, Hkv, D, cfg.p, cfg.L, cfg.k, q.dtype)
+    if lh.lh_check(pr) != lh.LH_OK:
+        raise SystemExit(f"invalid problem: {lh.lh_last_error()}")
+    S, Ptot = lh.lh_subseq_len(pr), lh.lh_pyramid_rows(pr)
+    R = Ptot - N
+    dt = q.dtype
+    es = q.element_size()
+    o = torch.empty_like(q)
+    idx = torch.empty(B, Hq, S, dtype=torch.int32, device=dev)
+    slot = torch.empty(B, Hq, Ptot, dtype=torch.int32, device=dev)
+    qs, ks, vs, os_ = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(4))
+    lse = torch.empty(B, Hq, S, dtype=torch.float32, device=dev)
+    dq = torch.empty_like(q)
+    dk = torch.empty_like(k)
+    dv = torch.empty_like(v)
+    wsf = lh.workspace(pr, lh.LH_OP_ATTENTION_FWD, dev)
+    wsb = lh.workspace(pr, lh.LH_OP_ATTENTION_BWD, dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        lh.lh_attention_fwd(pr, q, k, v, o, idx, slot, qs, ks, vs, os_, lse, wsf, stream=stream)
+        lh.lh_attention_bwd(pr, idx, slot, qs, ks, vs, os_, lse, dout, dq, dk, dv, wsb, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    print(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (host wall {wall / args.steps * 1e3:.3f} ms/step)",
+          file=sys.stderr, flush=True)
+
+    # ---- per-stage timing through the stage entry points (same kernels, same stream)
+    qp = torch.empty(B, R, Hq, D, dtype=dt, device=dev)
+    kp = torch.empty(B, R, Hkv, D, dtype=dt, device=dev)
+    vp = torch.empty_like(kp)
+    sqk = torch.empty(B, Hq, Ptot, dtype=torch.float32, device=dev)
+    skq = torch.empty(B, Hkv, Ptot, dtype=torch.float32, device=dev)
+    wss = lh.workspace(pr, lh.LH_OP_SELECT, dev)
+    wsd = lh.workspace(pr, lh.LH_OP_SDPA_BWD, dev)
+    dos, dqs, dks, dvs = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(4))
+    stages = {
+        "pool_score": lambda: (lh.lh_pyramid_pool(pr, q, k, v, qp, kp, vp, stream=stream),
+                               lh.lh_score(pr, q, k, sqk, skq, stream=stream)),
+        "select": lambda: lh.lh_select_topk(pr, sqk, skq, idx, slot, wss, stream=stream),
+        "gather": lambda: lh.lh_gather(pr, q, k, v, qp, kp, vp, idx, qs, ks, vs, stream=stream),
+        "sdpa_fwd": lambda: lh.lh_sdpa_fwd(pr, qs, ks, vs, os_, lse, stream=stream),
+        "scatter": lambda: lh.lh_scatter(pr, os_, slot, o, stream=stream),
+        "scatter_bwd": lambda: lh.lh_scatter_bwd(pr, dout, slot, dos, stream=stream),
+        "sdpa_bwd": lambda: lh.lh_sdpa_bwd(pr, qs, ks, vs, os_, lse, dos, dqs, dks, dvs, wsd, stream=stream),
+        "gather_bwd": lambda: lh.lh_gather_bwd(pr, dqs, dks, dvs, slot, dq, dk, dv, stream=stream),
+    }
+    work = stage_work(pr, S, Ptot, es)
+    per_stage = {}
+    reps = max(1, min(args.steps, 5))
+    for name, fn in stages.items():
+        fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        bound, amount = work[name]
+        if bound == "mfma":
+            ach = amount / (ms * 1e-3) / 1e12
+            per_stage[name] = dict(ms=round(ms, 4), tflops=round(ach, 2),
+                                   frac=round(ach / PEAK_BF16_TFLOPS, 4))
+        else:
+            ach = amount / (ms * 1e-3) / 1e9
+            per_stage[name] = dict(ms=round(ms, 4), gbs=round(ach, 1), frac=round(ach / PEAK_HBM_GBS, 4))
+        print(f"[bench] stage {name}: {per_stage[name]}", file=sys.stderr, flush=True)
+    dom = max(per_stage, key=lambda n: per_stage[n]["ms"])
+    bound, amount = work[dom]
+    ms = per_stage[dom]["ms"]
+    if bound == "mfma":
+        ach = amount / (ms * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(ach, 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                    frac=round(ach / PEAK_BF16_TFLOPS, 4), traffic=None, kernel=dom,
+                    per_launch=amount, per_launch_unit="FLOP")
+    else:
+        ach = amount / (ms * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s",
+                    frac=round(ach / PEAK_HBM_GBS, 4), traffic=None, kernel=dom,
+                    per_launch=amount, per_launch_unit="B")
+    mem_ms = sum(per_stage[n]["ms"] for n in per_stage if work[n][0] == "hbm")
+    mem_bytes = sum(work[n][1] for n in per_stage if work[n][0] == "hbm")
+    sdpa_ms = per_stage["sdpa_fwd"]["ms"] + per_stage["sdpa_bwd"]["ms"]
+    sdpa_flops = work["sdpa_fwd"][1] + work["sdpa_bwd"][1]
+    summary = dict(
+        stages=per_stage,
+        sdpa_frac_of_bf16_peak=round(sdpa_flops / (sdpa_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        memory_stages_frac_of_hbm=round(mem_bytes / (mem_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        S=S,
+    )
+    return ms_step, roof, summary, (B, N, Hq, Hkv, D, S)
+
+
+def cpu_baseline(cfg, shape, rows: int):
+    """The fp64 oracle on one query head of the workload (every stage in full, SDPA on the last
+    `rows` gathered rows), extrapolated to the whole layer by pair and head counts."""
+    import numpy as np
+    import oracle
+
+    B, N, Hq, Hkv, D, S_gpu = shape
+    inp = workloads.make_inputs(workloads.scaled(cfg, Hq=1, Hkv=1), device="cpu")
+    h = oracle.Head(cfg.N, cfg.D, cfg.p, cfg.L, cfg.k, oracle.BF16 if cfg.dtype == "bf16" else oracle.F32)
+    sc = 1.0 / math.sqrt(cfg.D)
+    q = inp["q"][0, :, 0, :].double().numpy()
+    k = inp["k"][0, :, 0, :].double().numpy()
+    v = inp["v"][0, :, 0, :].double().numpy()
+    dout = np.ascontiguousarray(inp["dout"][0, :, 0, :].double().numpy())
+    t0 = time.perf_counter()
+    s_qk, s_kq = oracle.scores(h, q), oracle.scores(h, k)
+    idx, slot = oracle.select(h, s_qk, s_kq)
+    qs = oracle.gather(h, oracle.pool(h, q), idx)
+    ks = oracle.gather(h, oracle.pool(h, k), idx)
+    vs = oracle.gather(h, oracle.pool(h, v), idx)
+    S = len(idx)
+    t_lin_fwd = time.perf_counter() - t0
+    r0 = S - rows
+    t0 = time.perf_counter()
+    os_, lse = oracle.sdpa_fwd(qs, ks, vs, sc, rows=(r0, S))
+    t_fwd = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    o = oracle.scatter(h, idx, os_)
+    dos = oracle.scatter_bwd(h, idx, dout)
+    t_lin_mid = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.sdpa_bwd(qs, ks, vs, os_, lse, dos, sc, qrows=(r0, S), krows=(S, S))
+    t_dq = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.sdpa_bwd(qs, ks, vs, os_, lse, dos, sc, qrows=(S, S), krows=(r0, S))
+    t_dk = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.gather_pool_bwd(h, idx, qs)
+    oracle.gather_pool_bwd(h, idx, ks)
+    oracle.gather_pool_bwd(h, idx, vs)
+    t_lin_bwd = time.perf_counter() - t0
+    # (query, key) pairs: fwd / dQ sample rows m in [r0, S) see m + 1 keys; dK/dV sample rows t
+    # in [r0, S) see S - t queries; the whole head has S (S + 1) / 2 pairs for each part
+    full_pairs = S * (S + 1) / 2
+    fwd_pairs = sum(m + 1 for m in range(r0, S))
+    dk_pairs = sum(S - t for t in range(r0, S))
+    t_head = (t_lin_fwd + t_lin_mid + t_lin_bwd + t_fwd * full_pairs / fwd_pairs
+              + t_dq * full_pairs / fwd_pairs + t_dk * full_pairs / dk_pairs)
+    t_layer = t_head * B * Hq
+    measured = t_lin_fwd + t_lin_mid + t_lin_bwd + t_fwd + t_dq + t_dk
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return dict(value=round(B * N / t_layer, 3), unit="tokens/s", cores=threads, kind="oracle",
+                sample=(f"one query head of the layer (pool, score, select, gather, scatter and their "
+                        f"adjoints in full; SDPA fwd, dQ and dK/dV on the last {rows} of S={S} gathered rows), "
+                        f"{measured:.1f} s measured, extrapolated by (query, key) pair counts and by "
+                        f"{B * Hq} heads; S check {S == S_gpu}"),
+                measured_s=round(measured, 2))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=512)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the layer runs on a single MI355X here; sharding it "
+              "over several GPUs (by KV-head group) is not built, so --gpus must be 1.",
+              file=sys.stderr)
+        raise SystemExit(2)
+    cfg = workloads.CONFIGS[args.config]
+    ms_step, roof, summary, shape = run_gpu(args, cfg)
+    B, N = shape[0], shape[1]
+    value = B * N / (ms_step * 1e-3)
+    line = dict(
+        metric="Lighthouse attn fwd+bwd tokens/s per layer at N=256K, 1 MI355X; % of peak",
+        value=round(value, 1), unit="tokens/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
+        ms_per_step=round(ms_step, 4), higher_is_better=True, scaling="weak", vs_baseline=None,
+        dtype="bf16" if cfg.dtype == "bf16" else "f32", data="synthetic",
+        config=dict(workload=(f"lighthouse layer fwd+bwd {cfg.name}: B={cfg.B} N={cfg.N} Hq={cfg.Hq} "
+                              f"Hkv={cfg.Hkv} D={cfg.D} p={cfg.p} L={cfg.L} k={cfg.k} S={summary['S']} "
+                              f"{cfg.dtype}, {cfg.structure} inputs"),
+                    global_batch=cfg.B, seq_len=cfg.N, parallelism="single-gpu"),
+        roofline=roof,
+        summary=summary,
+    )
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, shape, args.cpu_rows)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

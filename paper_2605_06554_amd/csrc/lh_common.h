@@ -1,0 +1,144 @@
+// lh_common.h -- device helpers shared by the Lighthouse HIP kernels (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/lighthouse.h"
+
+namespace lh {
+
+typedef uint16_t bf16_t;  // raw bf16 storage
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+struct alignas(16) u32x4 {
+  uint32_t x, y, z, w;
+};
+
+__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// fp32 -> bf16, round to nearest even (finite inputs).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  __bf16 b = (__bf16)f;
+  return __builtin_bit_cast(bf16_t, b);
+}
+
+// fp64 -> bf16 with a single rounding (nearest, ties to even): round to fp32 with
+// round-to-odd first (truncate, set the sticky bit when inexact); 24 >= 8 + 2 bits makes the
+// second rounding to bf16 exact-equivalent to rounding the fp64 value directly.
+__device__ __forceinline__ bf16_t f64_to_bf16(double d) {
+  float f = (float)d;
+  double back = (double)f;
+  if (back != d) {
+    uint32_t u = __float_as_uint(f);
+    if (fabs(back) > fabs(d)) u -= 1u;  // RNE rounded away from zero: step back toward zero
+    u |= 1u;
+    f = __uint_as_float(u);
+  }
+  return f2bf(f);
+}
+
+template <typename T>
+struct Elem;
+template <>
+struct Elem<float> {
+  static __device__ __forceinline__ float load(const float* p) { return *p; }
+  static __device__ __forceinline__ void store(float* p, float v) { *p = v; }
+  static __device__ __forceinline__ void store_f64(float* p, double v) { *p = (float)v; }
+};
+template <>
+struct Elem<bf16_t> {
+  static __device__ __forceinline__ float load(const bf16_t* p) { return bf2f(*p); }
+  static __device__ __forceinline__ void store(bf16_t* p, float v) { *p = f2bf(v); }
+  static __device__ __forceinline__ void store_f64(bf16_t* p, double v) { *p = f64_to_bf16(v); }
+};
+
+// 16-byte chunk of a row: 8 bf16 or 4 fp32 values.
+template <typename T>
+struct Chunk {
+  static constexpr int n = 16 / sizeof(T);
+};
+
+__device__ __forceinline__ void load_chunk_f32(const float* p, float* out4) {
+  float4 v = *reinterpret_cast<const float4*>(p);
+  out4[0] = v.x, out4[1] = v.y, out4[2] = v.z, out4[3] = v.w;
+}
+__device__ __forceinline__ void load_chunk_bf16(const bf16_t* p, float* out8) {
+  u32x4 v = *reinterpret_cast<const u32x4*>(p);
+  uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out8[2 * i] = __uint_as_float(w[i] << 16);
+    out8[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+template <typename T>
+__device__ __forceinline__ void load_chunk(const T* p, float* out);
+template <>
+__device__ __forceinline__ void load_chunk<float>(const float* p, float* out) { load_chunk_f32(p, out); }
+template <>
+__device__ __forceinline__ void load_chunk<bf16_t>(const bf16_t* p, float* out) { load_chunk_bf16(p, out); }
+
+__device__ __forceinline__ void store_chunk_f32(float* p, const float* v) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void store_chunk_bf16(bf16_t* p, const float* v) {
+  u32x4 o;
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(v[2 * i]) | ((uint32_t)f2bf(v[2 * i + 1]) << 16);
+  o.x = w[0], o.y = w[1], o.z = w[2], o.w = w[3];
+  *reinterpret_cast<u32x4*>(p) = o;
+}
+template <typename T>
+__device__ __forceinline__ void store_chunk(T* p, const float* v);
+template <>
+__device__ __forceinline__ void store_chunk<float>(float* p, const float* v) { store_chunk_f32(p, v); }
+template <>
+__device__ __forceinline__ void store_chunk<bf16_t>(bf16_t* p, const float* v) { store_chunk_bf16(p, v); }
+
+}  // namespace lh
+
+// ---------------------------------------------------------------- host-side launch interface
+// Shape facts computed on the host once per call and passed to every kernel launcher.
+struct LhShape {
+  int64_t B, N;
+  int32_t Hq, Hkv, D, p, L, k, G;  // G = Hq / Hkv
+  int32_t dtype;
+  float scale;
+  uint32_t flags;
+  int64_t Ptot, R, S;  // pyramid rows, pooled rows (Ptot - N), gathered length
+  int64_t P;           // p^(L-1)
+  int64_t pw[16];      // p^l
+  int64_t off[17];     // flattened offset of level l (off[L] = Ptot)
+  int64_t cand[16];    // candidates at level l (data independent)
+  int64_t npar[16];    // parents chosen at level l (>= 1), 0 at level 0
+  int64_t coff[17];    // offset of level l's candidate list in one head's workspace list
+  int64_t Scand;       // sum of cand[l]: ints of selection workspace per (b, hq)
+  int64_t maxsel;      // largest candidate count of a level that needs a real top-k
+};
+
+// Kernel launchers (each returns hipGetLastError() after enqueueing).
+hipError_t lh_launch_pool_score(const LhShape& s, const void* q, const void* k, const void* v,
+                                void* qpyr, void* kpyr, void* vpyr, float* s_qk, float* s_kq,
+                                hipStream_t st);
+hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_kq, int32_t* idx,
+                            int32_t* slot, int32_t* ws, hipStream_t st);
+hipError_t lh_launch_gather(const LhShape& s, const void* q, const void* k, const void* v,
+                            const void* qpyr, const void* kpyr, const void* vpyr,
+                            const int32_t* idx, void* qs, void* ks, void* vs, hipStream_t st);
+hipError_t lh_launch_scatter(const LhShape& s, const void* os, const int32_t* slot, void* o,
+                             hipStream_t st);
+hipError_t lh_launch_scatter_bwd(const LhShape& s, const void* dout, const int32_t* slot,
+                                 void* dos, hipStream_t st);
+hipError_t lh_launch_gather_bwd(const LhShape& s, const void* dqs, const void* dks,
+                                const void* dvs, const int32_t* slot, void* dq, void* dk,
+                                void* dv, hipStream_t st);
+hipError_t lh_launch_sdpa_fwd(const LhShape& s, const void* qs, const void* ks, const void* vs,
+                              void* os, float* lse, hipStream_t st);
+hipError_t lh_launch_sdpa_bwd(const LhShape& s, const void* qs, const void* ks, const void* vs,
+                              const void* os, const float* lse, const void* dos, void* dqs,
+                              void* dks, void* dvs, float* delta, hipStream_t st);

@@ -1,0 +1,119 @@
+"""Host-only checks of the C ABI: the library loads, exports every declared entry point, and its
+validation and shape math agree with the oracle (no device calls)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+import paper_2605_06554_amd as lh
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "lighthouse.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(lh_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(lh.library_path)
+    names = _declared()
+    assert len(names) >= 19
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(lh.EXPORTED) == names
+
+
+def _pr(**kw):
+    base = dict(B=1, N=1024, Hq=2, Hkv=2, D=64, p=4, L=3, k=128, dtype=lh.LH_F32)
+    base.update(kw)
+    return lh.problem(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(), 0),
+    (dict(N=1000), -2),                 # 16 does not divide 1000
+    (dict(p=1), -3),
+    (dict(L=0), -3),
+    (dict(L=9), -3),
+    (dict(k=-1), -3),
+    (dict(Hq=3, Hkv=2), -3),
+    (dict(D=96), -3),
+    (dict(dtype=7), -4),
+    (dict(flags=4), -3),
+    (dict(N=0), -2),
+    (dict(L=1, p=0), 0),                # p is irrelevant with one level
+    (dict(N=2 ** 20, L=2, k=1000), -3),  # one level would rank 262144 candidates
+])
+def test_check_codes(kw, code):
+    pr = _pr(**kw)
+    assert lh.lh_check(pr) == code
+    if code != 0:
+        assert lh.lh_last_error() != ""
+        assert lh.lh_subseq_len(pr) == -1
+
+
+def test_null_problem():
+    lib = ctypes.CDLL(lh.library_path)
+    lib.lh_check.argtypes = [ctypes.c_void_p]
+    assert lib.lh_check(None) == -1
+
+
+@pytest.mark.parametrize("name", list(workloads.CONFIGS) + list(workloads.TEST_CONFIGS))
+def test_shapes_match_oracle(name, rng):
+    c = {**workloads.CONFIGS, **workloads.TEST_CONFIGS}[name]
+    pr = lh.problem(c.B, c.N, c.Hq, c.Hkv, c.D, c.p, c.L, c.k, lh.LH_BF16, 0.0, c.flags)
+    assert lh.lh_check(pr) == 0
+    h = oracle.Head(c.N, c.D, c.p, c.L, c.k, oracle.F32, c.flags)
+    assert lh.lh_pyramid_rows(pr) == h.ptot
+    for l in range(c.L):
+        assert lh.lh_level_rows(pr, l) == h.level_rows(l)
+        assert lh.lh_level_offset(pr, l) == h.level_offset(l)
+    assert lh.lh_level_rows(pr, c.L) == -1
+    if h.ptot <= 400000:
+        s = rng.random(h.ptot).astype(np.float32)
+        idx, _ = oracle.select(h, s, s)
+        assert lh.lh_subseq_len(pr) == len(idx)
+
+
+@pytest.mark.parametrize("flags", [0, lh.LH_FLAG_REPLACE_PARENTS])
+@pytest.mark.parametrize("N,p,L,k", [(64, 2, 4, 3), (256, 4, 4, 300), (81, 3, 3, 4), (777, 4, 1, 0)])
+def test_subseq_len_matches_oracle_selection(N, p, L, k, flags, rng):
+    pr = lh.problem(1, N, 1, 1, 64, p, L, k, lh.LH_F32, 0.0, flags)
+    h = oracle.Head(N, 64, p, L, k, oracle.F32, flags)
+    s = rng.random(h.ptot).astype(np.float32)
+    idx, _ = oracle.select(h, s, s)
+    assert lh.lh_subseq_len(pr) == len(idx)
+
+
+def test_workspace_sizes():
+    c = workloads.CONFIGS["c4"]
+    pr = lh.problem(c.B, c.N, c.Hq, c.Hkv, c.D, c.p, c.L, c.k, lh.LH_BF16)
+    S = lh.lh_subseq_len(pr)
+    assert S == 54272
+    assert lh.lh_workspace_bytes(pr, lh.LH_OP_SDPA_BWD) >= c.B * c.Hq * S * 4
+    fwd = lh.lh_workspace_bytes(pr, lh.LH_OP_ATTENTION_FWD)
+    R = lh.lh_pyramid_rows(pr) - c.N
+    assert fwd >= (c.Hq + 2 * c.Hkv) * R * c.D * 2 + (c.Hq + c.Hkv) * lh.lh_pyramid_rows(pr) * 4
+    assert lh.lh_workspace_bytes(pr, lh.LH_OP_ATTENTION_BWD) >= 4 * c.Hq * S * c.D * 2
+    with pytest.raises(lh.LighthouseError):
+        lh.lh_workspace_bytes(pr, 99)
+
+
+def test_entry_points_reject_bad_pointers_before_any_launch():
+    # argument errors are caught on the host: no device is touched
+    pr = _pr()
+    lib = ctypes.CDLL(lh.library_path)
+    lib.lh_sdpa_fwd.argtypes = [ctypes.POINTER(lh.lh_problem)] + [ctypes.c_void_p] * 6
+    assert lib.lh_sdpa_fwd(ctypes.byref(pr), None, None, None, None, None, None) == -1
+    assert lib.lh_sdpa_fwd(ctypes.byref(pr), 0x1001, 0x2000, 0x3000, 0x4000, 0x5000, None) == -5
+    lib.lh_select_topk.argtypes = [ctypes.POINTER(lh.lh_problem)] + [ctypes.c_void_p] * 5 + [ctypes.c_size_t, ctypes.c_void_p]
+    assert lib.lh_select_topk(ctypes.byref(pr), 0x1000, 0x2000, 0x3000, 0x4000, None, 0, None) == -6
+    assert lib.lh_select_topk(ctypes.byref(pr), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 16, None) == -6
+    bad = _pr(N=1000)
+    assert lib.lh_sdpa_fwd(ctypes.byref(bad), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, None) == -2

@@ -1,0 +1,91 @@
+"""End-to-end parity of the fused layer (lh_attention_fwd / lh_attention_bwd) against the oracle,
+plus determinism and causality on the GPU."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from parity import check_close, check_close_heads, check_equal
+
+lh = pytest.importorskip("paper_2605_06554_amd")
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _cfg(name):
+    return {**workloads.CONFIGS, **workloads.TEST_CONFIGS}[name]
+
+
+def _run(c, inp):
+    q, k, v, dout = (inp[x].to(DEV) for x in ("q", "k", "v", "dout"))
+    pr, st = lh.attention_forward(q, k, v, c.p, c.L, c.k, flags=c.flags)
+    dq, dk, dv = lh.attention_backward(pr, st, dout)
+    torch.cuda.synchronize()
+    return pr, st, (dq, dk, dv)
+
+
+@pytest.mark.parametrize("name", ["c1", "t_gqa", "t_f32", "t_p3", "t_l1", "t_k0"])
+def test_layer_matches_oracle(name):
+    c = _cfg(name)
+    print(f"[e2e] {name}", flush=True)
+    inp = workloads.make_inputs(c)
+    pr, st, (dq, dk, dv) = _run(c, inp)
+    q, k, v = (inp[x].double().numpy() for x in ("q", "k", "v"))
+    odt = oracle.BF16 if c.dtype == "bf16" else oracle.F32
+    f = oracle.layer_forward(q, k, v, c.p, c.L, c.k, dtype=odt, flags=c.flags)
+    g = oracle.layer_backward(f, inp["dout"].double().numpy())
+    check_equal("idx", st["idx"], f["idx"])
+    check_equal("slot", st["slot"], f["slot"])
+    check_equal("qs", st["qs"].double(), f["qs"])
+    check_equal("ks", st["ks"].double(), f["ks"])
+    check_equal("vs", st["vs"].double(), f["vs"])
+    check_close_heads("os", st["os"], f["os"], c.dtype, 1)
+    check_close("lse", st["lse"], f["lse"], "fp32")
+    check_close_heads("o", st["o"], f["o"], c.dtype, 2)
+    check_close_heads("dq", dq, g["dq"], c.dtype, 2)
+    check_close_heads("dk", dk, g["dk"], c.dtype, 2)
+    check_close_heads("dv", dv, g["dv"], c.dtype, 2)
+
+
+def test_full_budget_replace_mode_is_dense_sdpa():
+    # replace mode with a budget covering everything leaves level 0 only: plain causal SDPA
+    c = workloads.scaled(workloads.TEST_CONFIGS["t_gqa"], N=1024, k=1024, flags=lh.LH_FLAG_REPLACE_PARENTS)
+    inp = workloads.make_inputs(c)
+    pr, st, (dq, dk, dv) = _run(c, inp)
+    assert lh.lh_subseq_len(pr) == c.N
+    assert st["idx"][0, 0].cpu().tolist() == list(range(c.N))
+    G = c.Hq // c.Hkv
+    qf, kf, vf = (inp[x].float().transpose(1, 2) for x in ("q", "k", "v"))
+    kf, vf = kf.repeat_interleave(G, 1), vf.repeat_interleave(G, 1)
+    ref = torch.nn.functional.scaled_dot_product_attention(qf.double(), kf.double(), vf.double(), is_causal=True)
+    check_close("o", st["o"].transpose(1, 2), ref.numpy(), "bf16")
+
+
+def test_deterministic():
+    c = _cfg("t_gqa")
+    inp = workloads.make_inputs(c)
+    _, s1, g1 = _run(c, inp)
+    _, s2, g2 = _run(c, inp)
+    for key in ("idx", "slot", "qs", "os", "lse", "o"):
+        assert torch.equal(s1[key], s2[key]), key
+    for a, b in zip(g1, g2):
+        assert torch.equal(a, b)
+
+
+def test_causality_on_gpu():
+    # sign flips of Q/K rows and new V rows after position t leave the selection (norms) and
+    # every output up to t unchanged
+    c = _cfg("t_gqa")
+    inp = workloads.make_inputs(c)
+    _, s1, _ = _run(c, inp)
+    t = 2500
+    inp2 = {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+    inp2["q"][:, t + 1:] *= -1
+    inp2["k"][:, t + 1:] *= -1
+    inp2["v"][:, t + 1:] = torch.randn_like(inp2["v"][:, t + 1:].float()).to(inp2["v"].dtype)
+    _, s2, _ = _run(c, inp2)
+    assert torch.equal(s1["idx"], s2["idx"])
+    assert torch.equal(s1["o"][:, : t + 1], s2["o"][:, : t + 1])
+    assert not torch.equal(s1["o"][:, t + 1:], s2["o"][:, t + 1:])

@@ -1,0 +1,235 @@
+"""Per-stage parity of the HIP path against the oracle (small shapes, several tiles, ragged
+tails). Every call goes through the C ABI."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from parity import check_close, check_equal, to64
+
+lh = pytest.importorskip("paper_2605_06554_amd")
+
+pytestmark = pytest.mark.gpu
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+DEV = "cuda"
+
+
+def _cfg(name):
+    return {**workloads.CONFIGS, **workloads.TEST_CONFIGS}[name]
+
+
+def _problem(c, **kw):
+    d = dict(B=c.B, N=c.N, Hq=c.Hq, Hkv=c.Hkv, D=c.D, p=c.p, L=c.L, k=c.k,
+             dtype=lh.LH_BF16 if c.dtype == "bf16" else lh.LH_F32, scale=0.0, flags=c.flags)
+    d.update(kw)
+    return lh.problem(**d)
+
+
+def _odt(c):
+    return oracle.BF16 if c.dtype == "bf16" else oracle.F32
+
+
+STAGE_CFGS = ["c1", "t_gqa", "t_f32", "t_p3", "t_k0"]
+
+
+@pytest.mark.parametrize("name", STAGE_CFGS + ["t_l1"])
+def test_pool_and_score(name):
+    c = _cfg(name)
+    print(f"[stage pool/score] {name}", flush=True)
+    inp = workloads.make_inputs(c, with_grad=False)
+    pr = _problem(c)
+    Ptot = lh.lh_pyramid_rows(pr)
+    R = Ptot - c.N
+    q, k, v = (inp[x].to(DEV) for x in ("q", "k", "v"))
+    dt = q.dtype
+    qp = torch.empty(c.B, max(R, 1), c.Hq, c.D, dtype=dt, device=DEV)
+    kp = torch.empty(c.B, max(R, 1), c.Hkv, c.D, dtype=dt, device=DEV)
+    vp = torch.empty_like(kp)
+    sqk = torch.empty(c.B, c.Hq, Ptot, dtype=torch.float32, device=DEV)
+    skq = torch.empty(c.B, c.Hkv, Ptot, dtype=torch.float32, device=DEV)
+    lh.lh_pyramid_pool(pr, q, k, v, qp, kp, vp)
+    lh.lh_score(pr, q, k, sqk, skq)
+    torch.cuda.synchronize()
+    h = oracle.Head(c.N, c.D, c.p, c.L, c.k, _odt(c))
+    for b in range(c.B):
+        for hh in range(c.Hq):
+            x = inp["q"][b, :, hh, :].double().numpy()
+            check_equal(f"s_qk[{b},{hh}]", sqk[b, hh], oracle.scores(h, x))
+            if R > 0:
+                check_equal(f"qpyr[{b},{hh}]", to64(qp[b, :, hh]), oracle.pool(h, x)[c.N:])
+        for hh in range(c.Hkv):
+            xk = inp["k"][b, :, hh, :].double().numpy()
+            xv = inp["v"][b, :, hh, :].double().numpy()
+            check_equal(f"s_kq[{b},{hh}]", skq[b, hh], oracle.scores(h, xk))
+            if R > 0:
+                check_equal(f"kpyr[{b},{hh}]", to64(kp[b, :, hh]), oracle.pool(h, xk)[c.N:])
+                check_equal(f"vpyr[{b},{hh}]", to64(vp[b, :, hh]), oracle.pool(h, xv)[c.N:])
+
+
+def _run_select(pr, sqk, skq):
+    S, Ptot = lh.lh_subseq_len(pr), lh.lh_pyramid_rows(pr)
+    idx = torch.empty(pr.B, pr.Hq, S, dtype=torch.int32, device=DEV)
+    slot = torch.empty(pr.B, pr.Hq, Ptot, dtype=torch.int32, device=DEV)
+    ws = lh.workspace(pr, lh.LH_OP_SELECT)
+    lh.lh_select_topk(pr, sqk, skq, idx, slot, ws)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), slot.cpu().numpy()
+
+
+def test_select_fig2_toy():
+    g = json.load(open(os.path.join(GOLD, "fig2_selection.json")))
+    pr = lh.problem(1, g["N"], 1, 1, 64, g["p"], g["L"], g["k"], lh.LH_F32)
+    Ptot = lh.lh_pyramid_rows(pr)
+    s = np.zeros(Ptot, np.float32)
+    off1, off2 = lh.lh_level_offset(pr, 1), lh.lh_level_offset(pr, 2)
+    s[off2: off2 + 4] = g["level2_scores"]
+    for i, v in zip(g["level1_candidates"], g["level1_scores"]):
+        s[off1 + i] = v
+    sq = torch.from_numpy(s).view(1, 1, Ptot).to(DEV)
+    sk = torch.zeros_like(sq)
+    idx, slot = _run_select(pr, sq, sk)
+    assert idx[0, 0].tolist() == g["idx"]
+    assert all(slot[0, 0, t] == m for m, t in enumerate(g["idx"]))
+    assert (slot >= 0).sum() == g["S"]
+
+
+@pytest.mark.parametrize("ties", [False, True])
+@pytest.mark.parametrize("N,p,L,k,flags", [(4096, 4, 4, 100, 0), (4096, 4, 4, 100, 1), (2048, 2, 6, 37, 0),
+                                           (2187, 3, 3, 50, 1), (16384, 4, 5, 4096, 0), (65536, 4, 3, 8192, 0)])
+def test_select_random_scores(N, p, L, k, flags, ties, rng):
+    Hq, Hkv = 4, 2
+    print(f"[stage select] N={N} p={p} L={L} k={k} flags={flags} ties={ties}", flush=True)
+    pr = lh.problem(2, N, Hq, Hkv, 64, p, L, k, lh.LH_F32, 0.0, flags)
+    Ptot = lh.lh_pyramid_rows(pr)
+    if ties:
+        sq = rng.integers(0, 5, (2, Hq, Ptot)).astype(np.float32)
+        sk = rng.integers(0, 5, (2, Hkv, Ptot)).astype(np.float32)
+    else:
+        sq = rng.random((2, Hq, Ptot)).astype(np.float32)
+        sk = rng.random((2, Hkv, Ptot)).astype(np.float32)
+    idx, slot = _run_select(pr, torch.from_numpy(sq).to(DEV), torch.from_numpy(sk).to(DEV))
+    h = oracle.Head(N, 64, p, L, k, oracle.F32, flags)
+    for b in range(2):
+        for hq in range(Hq):
+            ri, rs = oracle.select(h, sq[b, hq], sk[b, hq // 2])
+            check_equal(f"idx[{b},{hq}]", idx[b, hq], ri)
+            check_equal(f"slot[{b},{hq}]", slot[b, hq], rs)
+
+
+def _layer_oracle(c, inp):
+    q, k, v = (inp[x].double().numpy() for x in ("q", "k", "v"))
+    return oracle.layer_forward(q, k, v, c.p, c.L, c.k, dtype=_odt(c), flags=c.flags)
+
+
+@pytest.mark.parametrize("name", STAGE_CFGS)
+def test_gather_sdpa_scatter_stages(name):
+    c = _cfg(name)
+    print(f"[stage gather/sdpa/scatter] {name}", flush=True)
+    inp = workloads.make_inputs(c)
+    f = _layer_oracle(c, inp)
+    g = oracle.layer_backward(f, inp["dout"].double().numpy())
+    pr = _problem(c)
+    S, Ptot = lh.lh_subseq_len(pr), lh.lh_pyramid_rows(pr)
+    R = Ptot - c.N
+    dt = inp["q"].dtype
+    q, k, v, dout = (inp[x].to(DEV) for x in ("q", "k", "v", "dout"))
+    qp = torch.empty(c.B, max(R, 1), c.Hq, c.D, dtype=dt, device=DEV)
+    kp = torch.empty(c.B, max(R, 1), c.Hkv, c.D, dtype=dt, device=DEV)
+    vp = torch.empty_like(kp)
+    lh.lh_pyramid_pool(pr, q, k, v, qp, kp, vp)
+    idx = torch.from_numpy(f["idx"].astype(np.int32)).to(DEV)
+    slot = torch.from_numpy(f["slot"].astype(np.int32)).to(DEV)
+    qs, ks, vs, os_ = (torch.empty(c.B, c.Hq, S, c.D, dtype=dt, device=DEV) for _ in range(4))
+    lh.lh_gather(pr, q, k, v, qp, kp, vp, idx, qs, ks, vs)
+    torch.cuda.synchronize()
+    check_equal("qs", to64(qs), f["qs"])
+    check_equal("ks", to64(ks), f["ks"])
+    check_equal("vs", to64(vs), f["vs"])
+    lse = torch.empty(c.B, c.Hq, S, dtype=torch.float32, device=DEV)
+    lh.lh_sdpa_fwd(pr, qs, ks, vs, os_, lse)
+    torch.cuda.synchronize()
+    for b in range(c.B):
+        for hq in range(c.Hq):
+            check_close(f"os[{b},{hq}]", os_[b, hq], f["os"][b, hq], c.dtype)
+    check_close("lse", lse, f["lse"], "fp32")
+    # scatter of the oracle's own sub-sequence output (rounded to the dtype) isolates the scatter
+    os_ref = torch.from_numpy(f["os"]).to(dt).to(DEV)
+    o = torch.empty_like(q)
+    lh.lh_scatter(pr, os_ref, slot, o)
+    torch.cuda.synchronize()
+    h = f["head"]
+    for b in range(c.B):
+        for hq in range(c.Hq):
+            ref = oracle.scatter(h, f["idx"][b, hq], to64(os_ref[b, hq]))
+            check_close(f"o[{b},{hq}]", o[b, :, hq], ref, c.dtype)
+    dos = torch.empty(c.B, c.Hq, S, c.D, dtype=dt, device=DEV)
+    lh.lh_scatter_bwd(pr, dout, slot, dos)
+    torch.cuda.synchronize()
+    for b in range(c.B):
+        for hq in range(c.Hq):
+            check_close(f"dos[{b},{hq}]", dos[b, hq], g["dos"][b, hq], c.dtype)
+    # SDPA backward on the oracle's inputs (os/lse from the GPU forward)
+    dqs, dks, dvs = (torch.empty(c.B, c.Hq, S, c.D, dtype=dt, device=DEV) for _ in range(3))
+    dos_ref = torch.from_numpy(g["dos"]).to(dt).to(DEV)
+    ws = lh.workspace(pr, lh.LH_OP_SDPA_BWD)
+    lh.lh_sdpa_bwd(pr, qs, ks, vs, os_, lse, dos_ref, dqs, dks, dvs, ws)
+    torch.cuda.synchronize()
+    sc = f["scale"]
+    for b in range(c.B):
+        for hq in range(c.Hq):
+            rq, rk, rv = oracle.sdpa_bwd(f["qs"][b, hq], f["ks"][b, hq], f["vs"][b, hq], f["os"][b, hq],
+                                         f["lse"][b, hq], to64(dos_ref[b, hq]), sc)
+            check_close(f"dqs[{b},{hq}]", dqs[b, hq], rq, c.dtype)
+            check_close(f"dks[{b},{hq}]", dks[b, hq], rk, c.dtype)
+            check_close(f"dvs[{b},{hq}]", dvs[b, hq], rv, c.dtype)
+    # gather + pool backward on the oracle's sub-sequence gradients
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    dqs_r, dks_r, dvs_r = (torch.from_numpy(g[x]).to(dt).to(DEV) for x in ("dqs", "dks", "dvs"))
+    lh.lh_gather_bwd(pr, dqs_r, dks_r, dvs_r, slot, dq, dk, dv)
+    torch.cuda.synchronize()
+    G = c.Hq // c.Hkv
+    for b in range(c.B):
+        for hq in range(c.Hq):
+            ref = oracle.gather_pool_bwd(h, f["idx"][b, hq], to64(dqs_r[b, hq]))
+            check_close(f"dq[{b},{hq}]", dq[b, :, hq], ref, c.dtype)
+        for gg in range(c.Hkv):
+            rk = np.zeros((c.N, c.D))
+            rv = np.zeros((c.N, c.D))
+            for hq in range(gg * G, (gg + 1) * G):
+                oracle.gather_pool_bwd(h, f["idx"][b, hq], to64(dks_r[b, hq]), rk)
+                oracle.gather_pool_bwd(h, f["idx"][b, hq], to64(dvs_r[b, hq]), rv)
+            check_close(f"dk[{b},{gg}]", dk[b, :, gg], rk, c.dtype)
+            check_close(f"dv[{b},{gg}]", dv[b, :, gg], rv, c.dtype)
+
+
+@pytest.mark.parametrize("S,D,dt", [(1, 128, "bf16"), (31, 64, "bf16"), (300, 128, "bf16"), (1000, 64, "bf16"),
+                                    (2113, 128, "bf16"), (257, 64, "fp32"), (700, 128, "fp32")])
+def test_sdpa_standalone(S, D, dt, rng):
+    print(f"[stage sdpa] S={S} D={D} {dt}", flush=True)
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    B, H = 1, 2
+    pr = lh.problem(B, S, H, H, D, 2, 1, 0, tdt)  # L = 1: S rows
+    assert lh.lh_subseq_len(pr) == S
+    x = [torch.from_numpy(rng.standard_normal((B, H, S, D))).to(tdt) for _ in range(4)]
+    qs, ks, vs, dos = (t.to(DEV) for t in x)
+    os_ = torch.empty_like(qs)
+    lse = torch.empty(B, H, S, dtype=torch.float32, device=DEV)
+    lh.lh_sdpa_fwd(pr, qs, ks, vs, os_, lse)
+    dqs, dks, dvs = torch.empty_like(qs), torch.empty_like(qs), torch.empty_like(qs)
+    ws = lh.workspace(pr, lh.LH_OP_SDPA_BWD)
+    lh.lh_sdpa_bwd(pr, qs, ks, vs, os_, lse, dos, dqs, dks, dvs, ws)
+    torch.cuda.synchronize()
+    sc = 1.0 / np.sqrt(D)
+    for hh in range(H):
+        a = [t[0, hh].double().numpy() for t in x]
+        ro, rl = oracle.sdpa_fwd(a[0], a[1], a[2], sc)
+        check_close(f"os[{hh}]", os_[0, hh], ro, dt)
+        check_close(f"lse[{hh}]", lse[0, hh], rl, "fp32")
+        rq, rk, rv = oracle.sdpa_bwd(a[0], a[1], a[2], ro, rl, a[3], sc)
+        check_close(f"dqs[{hh}]", dqs[0, hh], rq, dt)
+        check_close(f"dks[{hh}]", dks[0, hh], rk, dt)
+        check_close(f"dvs[{hh}]", dvs[0, hh], rv, dt)
