@@ -64,17 +64,79 @@ __device__ __forceinline__ bf16x8 tr_operand(const bf16_t* mat, int stride, int 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-// ------------------------------------------------------------------ bf16 forward
-constexpr int FQ = 128;  // query rows per workgroup (4 waves x 32)
-constexpr int FK = 64;   // keys per tile
+// ------------------------------------------------------------------ tiles in LDS
+// A tile is TR rows of D bf16 values (D * 2 bytes per row, no padding). 16-byte chunk c of
+// row r is stored at chunk position c ^ swz(r), swz(r) = 2 (r % 8) masked to the D / 8 chunks
+// of a row: consecutive rows reading the same logical chunk hit different chunk positions (no
+// bank conflicts for b128 reads), and the XOR with an even value keeps chunk pairs (2m, 2m+1)
+// adjacent and in order, so the 32-byte row segments of the transposed loads stay intact.
+template <int D>
+__device__ __forceinline__ int swz(int r) { return ((r & 7) << 1) & (D / 8 - 1); }
 
 template <int D>
-__global__ void __launch_bounds__(256) sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K,
-                                                     const bf16_t* __restrict__ V, bf16_t* __restrict__ O,
-                                                     float* __restrict__ LSE, int64_t S, float sl2) {
-  constexpr int KST = D + 8, VST = D + 16;
-  __shared__ __align__(16) bf16_t Ks[FK * KST];
-  __shared__ __align__(16) bf16_t Vs[FK * VST];
+__device__ __forceinline__ int tile_off(int r, int col) {  // element offset of (row, col)
+  return r * D + ((((col >> 3) ^ swz<D>(r))) << 3) + (col & 7);
+}
+
+// Direct global -> LDS copy of TR rows starting at row r0 of a [S, D] bf16 matrix into a
+// swizzled tile, by the NW waves of the block. Each wave instruction writes 1 KB of LDS
+// contiguously (lane i -> byte 16 i), so every lane fetches the logical chunk that belongs at
+// its physical position. Rows past S are clamped to row S - 1 (callers mask them).
+template <int D, int TR, int NW>
+__device__ __forceinline__ void load_tile_lds(bf16_t* tile, const bf16_t* src, int64_t r0, int64_t S, int w, int lane) {
+  constexpr int CPR = D / 8;                 // chunks per row
+  constexpr int PER_WAVE = TR * CPR / 64;    // wave instructions per tile
+  static_assert(TR * CPR % (64 * NW) == 0, "tile must split evenly over the waves");
+#pragma unroll
+  for (int j = 0; j < PER_WAVE / NW; ++j) {
+    const int blk = w * (PER_WAVE / NW) + j;   // 1 KB block of the tile
+    const int pos = blk * 64 + lane;           // physical chunk index in the tile
+    const int r = pos / CPR, pc = pos % CPR;
+    const int c = pc ^ swz<D>(r);
+    int64_t gr = r0 + r;
+    if (gr > S - 1) gr = S - 1;
+    const bf16_t* g = src + gr * D + c * 8;
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
+                                     (__attribute__((address_space(3))) void*)(tile + blk * 512), 16, 0, 0);
+  }
+}
+
+// MFMA operand: 8 consecutive columns (16 bytes) of one tile row.
+template <int D>
+__device__ __forceinline__ bf16x8 tile_row8(const bf16_t* tile, int r, int col) {
+  return *reinterpret_cast<const bf16x8*>(tile + tile_off<D>(r, col));
+}
+
+// Transposed operand from a swizzled tile: slots 0-3 are rows r16 + 4h + 0..3 and slots 4-7 are
+// rows r16 + 8 + 4h + 0..3; column c32 + lane % 32 (see tr_read).
+template <int D>
+__device__ __forceinline__ bf16x8 tile_tr8(const bf16_t* tile, int r16, int c32, int lane) {
+  const int h = lane >> 5;
+  const int row = r16 + 4 * h + ((lane & 15) >> 2);
+  const int col = c32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const s16x4 lo = tr_read(tile + tile_off<D>(row, col));
+  const s16x4 hi = tr_read(tile + tile_off<D>(row + 8, col));
+  return cat8(lo, hi);
+}
+
+__device__ __forceinline__ bf16x8 cvt8(const float* f) {
+  typedef __attribute__((__vector_size__(8 * sizeof(float)))) float f32x8;
+  f32x8 v = {f[0], f[1], f[2], f[3], f[4], f[5], f[6], f[7]};
+  return __builtin_convertvector(v, bf16x8);
+}
+
+// ------------------------------------------------------------------ bf16 forward
+constexpr int FW = 8;         // waves per workgroup
+constexpr int FQ = 32 * FW;   // query rows per workgroup
+constexpr int FK = 64;        // keys per tile
+constexpr float kRescale = 8.0f;  // lazy rescaling threshold (log2 units)
+
+template <int D>
+__global__ void __launch_bounds__(64 * FW) __attribute__((amdgpu_waves_per_eu(2, 2)))
+sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
+              bf16_t* __restrict__ O, float* __restrict__ LSE, int64_t S, float sl2) {
+  __shared__ __align__(16) bf16_t Ks[2][FK * D];
+  __shared__ __align__(16) bf16_t Vs[2][FK * D];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int h = lane >> 5, r32 = lane & 31;
   const int64_t bh = blockIdx.y;
@@ -86,90 +148,82 @@ __global__ void __launch_bounds__(256) sdpa_fwd_bf16(const bf16_t* __restrict__ 
   const bf16_t* Kh = K + bh * S * D;
   const bf16_t* Vh = V + bh * S * D;
 
+  int64_t kend = q0 + FQ;
+  if (kend > S) kend = S;
+  const int nkt = (int)((kend + FK - 1) / FK);
+  load_tile_lds<D, FK, FW>(Ks[0], Kh, 0, S, w, lane);
+  load_tile_lds<D, FK, FW>(Vs[0], Vh, 0, S, w, lane);
+
   bf16x8 qreg[D / 16];
+  const int64_t qrow = myq < S ? myq : S - 1;
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
-    if (myq < S) qreg[kk] = ld8(Qh + myq * D + 16 * kk + 8 * h);
-    else qreg[kk] = bf16x8{};
-  }
+  for (int kk = 0; kk < D / 16; ++kk) qreg[kk] = ld8(Qh + qrow * D + 16 * kk + 8 * h);
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int d = 0; d < D / 32; ++d) oacc[d] = f32x16{};
   float m_run = -INFINITY, l_run = 0.0f;
 
-  int64_t kend = q0 + FQ;
-  if (kend > S) kend = S;
-  const int nkt = (int)((kend + FK - 1) / FK);
   for (int kt = 0; kt < nkt; ++kt) {
-    const int64_t k0 = (int64_t)kt * FK;
-    for (int c = tid; c < FK * (D / 8); c += 256) {
-      const int r = c / (D / 8), cc = c % (D / 8);
-      const int64_t key = k0 + r;
-      u32x4 kv{0, 0, 0, 0}, vv{0, 0, 0, 0};
-      if (key < S) {
-        kv = *reinterpret_cast<const u32x4*>(Kh + key * D + cc * 8);
-        vv = *reinterpret_cast<const u32x4*>(Vh + key * D + cc * 8);
-      }
-      *reinterpret_cast<u32x4*>(Ks + r * KST + cc * 8) = kv;
-      *reinterpret_cast<u32x4*>(Vs + r * VST + cc * 8) = vv;
+    const int buf = kt & 1;
+    __syncthreads();  // tile kt landed (the wait precedes the barrier); buffer buf^1 is free
+    if (kt + 1 < nkt) {
+      load_tile_lds<D, FK, FW>(Ks[buf ^ 1], Kh, (int64_t)(kt + 1) * FK, S, w, lane);
+      load_tile_lds<D, FK, FW>(Vs[buf ^ 1], Vh, (int64_t)(kt + 1) * FK, S, w, lane);
     }
-    __syncthreads();
-    if (qw + 31 >= k0) {
-      f32x16 sacc[2] = {f32x16{}, f32x16{}};
+    const int64_t k0 = (int64_t)kt * FK;
+    if (qw + 31 < k0) continue;  // every key of this tile is in the future of this wave's rows
+    const bf16_t* Kt = Ks[buf];
+    const bf16_t* Vt = Vs[buf];
+    f32x16 sacc[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk)
-          sacc[kb] = mfma32(ld8(Ks + (kb * 32 + r32) * KST + 16 * kk + 8 * h), qreg[kk], sacc[kb]);
-      const bool diag = k0 + FK - 1 > qw;
-      float mloc = -INFINITY;
+        sacc[kb] = mfma32(tile_row8<D>(Kt, kb * 32 + r32, 16 * kk + 8 * h), qreg[kk], sacc[kb]);
+    if (k0 + FK - 1 > qw) {  // diagonal tile: mask keys after the row
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          float s = sacc[kb][i] * sl2;
           const int64_t key = k0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-          if (diag && key > myq) s = -INFINITY;
-          sacc[kb][i] = s;
-          mloc = fmaxf(mloc, s);
+          if (key > myq) sacc[kb][i] = -INFINITY;
         }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float m_new = fmaxf(m_run, mloc);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      float rs = 0.0f;
+    }
+    float mloc = sacc[0][0];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float pv = __builtin_amdgcn_exp2f(sacc[kb][i] - m_new);
-          sacc[kb][i] = pv;
-          rs += pv;
-        }
-      rs += __shfl_xor(rs, 32, 64);
-      l_run = l_run * alpha + rs;
-      m_run = m_new;
+      for (int i = 0; i < 16; ++i) mloc = fmaxf(mloc, sacc[kb][i]);
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * sl2;
+    if (mloc > m_run + kRescale) {  // new running max: rescale what was accumulated so far
+      const float alpha = __builtin_amdgcn_exp2f(m_run - mloc);
+      l_run *= alpha;
 #pragma unroll
       for (int d = 0; d < D / 32; ++d)
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[d][i] *= alpha;
-      bf16x8 pb[4];
+      m_run = mloc;
+    }
+    bf16x8 pb[4];
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        float f[8];
+    for (int s = 0; s < 4; ++s) {
+      float f[8];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) f[t] = sacc[s >> 1][8 * (s & 1) + t];
-        pb[s] = pack8(f);
+      for (int t = 0; t < 8; ++t) {
+        f[t] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[s >> 1][8 * (s & 1) + t], sl2, -m_run));
+        l_run += f[t];
       }
+      pb[s] = cvt8(f);
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int d = 0; d < D / 32; ++d)
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-          oacc[d] = mfma32(tr_operand(Vs, VST, 16 * s, 32 * d, lane), pb[s], oacc[d]);
-    }
-    __syncthreads();
+        oacc[d] = mfma32(tile_tr8<D>(Vt, 16 * s, 32 * d, lane), pb[s], oacc[d]);
   }
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (myq < S) {
-    const float inv = 1.0f / l_run;
+    const float inv = 1.0f / l_tot;
     bf16_t* Oh = O + bh * S * D + myq * D;
 #pragma unroll
     for (int d = 0; d < D / 32; ++d)
@@ -180,7 +234,7 @@ __global__ void __launch_bounds__(256) sdpa_fwd_bf16(const bf16_t* __restrict__ 
         uint32_t w1 = (uint32_t)f2bf(oacc[d][4 * g4 + 2] * inv) | ((uint32_t)f2bf(oacc[d][4 * g4 + 3] * inv) << 16);
         *reinterpret_cast<uint2*>(Oh + col) = make_uint2(w0, w1);
       }
-    if (h == 0) LSE[bh * S + myq] = (m_run + __log2f(l_run)) * kLn2;
+    if (h == 0) LSE[bh * S + myq] = (m_run + __log2f(l_tot)) * kLn2;
   }
 }
 
@@ -206,17 +260,21 @@ __global__ void __launch_bounds__(256) sdpa_delta(const T* __restrict__ O, const
 }
 
 // ------------------------------------------------------------------ bf16 backward: dQ
-constexpr int BQ = 128;  // queries per workgroup in the dQ kernel
-constexpr int BK = 64;   // keys per tile in the dQ kernel
+// Each wave owns 32 query rows (its Q and dO rows stay in registers) and streams double-
+// buffered K/V tiles: S^T = K Q^T and dP^T = V dO^T give, per lane, one query row's
+// P = exp2(S scale log2e - lse log2e) and dS = P (dP - Delta); dQ^T += K^T dS^T with the
+// transposed K operand read from the same LDS tile.
+constexpr int QW = 8;        // waves per workgroup (dQ)
+constexpr int BQ = 32 * QW;  // query rows per workgroup
+constexpr int BK = 64;       // keys per tile
 
 template <int D>
-__global__ void __launch_bounds__(256) sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K,
-                                                        const bf16_t* __restrict__ V, const bf16_t* __restrict__ dO,
-                                                        const float* __restrict__ LSE, const float* __restrict__ DELTA,
-                                                        bf16_t* __restrict__ dQ, int64_t S, float sl2, float scale) {
-  constexpr int ST = D + 8;
-  __shared__ __align__(16) bf16_t Ks[BK * ST];
-  __shared__ __align__(16) bf16_t Vs[BK * ST];
+__global__ void __launch_bounds__(64 * QW) __attribute__((amdgpu_waves_per_eu(2, 2)))
+sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
+                 const bf16_t* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ DELTA,
+                 bf16_t* __restrict__ dQ, int64_t S, float sl2, float scale) {
+  __shared__ __align__(16) bf16_t Ks[2][BK * D];
+  __shared__ __align__(16) bf16_t Vs[2][BK * D];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int h = lane >> 5, r32 = lane & 31;
   const int64_t bh = blockIdx.y;
@@ -229,16 +287,18 @@ __global__ void __launch_bounds__(256) sdpa_bwd_dq_bf16(const bf16_t* __restrict
   const bf16_t* Vh = V + bh * S * D;
   const bf16_t* dOh = dO + bh * S * D;
 
+  int64_t kend = q0 + BQ;
+  if (kend > S) kend = S;
+  const int nkt = (int)((kend + BK - 1) / BK);
+  load_tile_lds<D, BK, QW>(Ks[0], Kh, 0, S, w, lane);
+  load_tile_lds<D, BK, QW>(Vs[0], Vh, 0, S, w, lane);
+
+  const int64_t qrow = myq < S ? myq : S - 1;
   bf16x8 qreg[D / 16], doreg[D / 16];
 #pragma unroll
   for (int kk = 0; kk < D / 16; ++kk) {
-    if (myq < S) {
-      qreg[kk] = ld8(Qh + myq * D + 16 * kk + 8 * h);
-      doreg[kk] = ld8(dOh + myq * D + 16 * kk + 8 * h);
-    } else {
-      qreg[kk] = bf16x8{};
-      doreg[kk] = bf16x8{};
-    }
+    qreg[kk] = ld8(Qh + qrow * D + 16 * kk + 8 * h);
+    doreg[kk] = ld8(dOh + qrow * D + 16 * kk + 8 * h);
   }
   const float lse2 = myq < S ? LSE[bh * S + myq] * kLog2e : INFINITY;
   const float dlt = myq < S ? DELTA[bh * S + myq] : 0.0f;
@@ -246,57 +306,45 @@ __global__ void __launch_bounds__(256) sdpa_bwd_dq_bf16(const bf16_t* __restrict
 #pragma unroll
   for (int d = 0; d < D / 32; ++d) dqacc[d] = f32x16{};
 
-  int64_t kend = q0 + BQ;
-  if (kend > S) kend = S;
-  const int nkt = (int)((kend + BK - 1) / BK);
   for (int kt = 0; kt < nkt; ++kt) {
-    const int64_t k0 = (int64_t)kt * BK;
-    for (int c = tid; c < BK * (D / 8); c += 256) {
-      const int r = c / (D / 8), cc = c % (D / 8);
-      const int64_t key = k0 + r;
-      u32x4 kv{0, 0, 0, 0}, vv{0, 0, 0, 0};
-      if (key < S) {
-        kv = *reinterpret_cast<const u32x4*>(Kh + key * D + cc * 8);
-        vv = *reinterpret_cast<const u32x4*>(Vh + key * D + cc * 8);
-      }
-      *reinterpret_cast<u32x4*>(Ks + r * ST + cc * 8) = kv;
-      *reinterpret_cast<u32x4*>(Vs + r * ST + cc * 8) = vv;
-    }
+    const int buf = kt & 1;
     __syncthreads();
-    if (qw + 31 >= k0) {
-      f32x16 sacc[2] = {f32x16{}, f32x16{}}, pacc[2] = {f32x16{}, f32x16{}};
+    if (kt + 1 < nkt) {
+      load_tile_lds<D, BK, QW>(Ks[buf ^ 1], Kh, (int64_t)(kt + 1) * BK, S, w, lane);
+      load_tile_lds<D, BK, QW>(Vs[buf ^ 1], Vh, (int64_t)(kt + 1) * BK, S, w, lane);
+    }
+    const int64_t k0 = (int64_t)kt * BK;
+    if (qw + 31 < k0) continue;
+    const bf16_t* Kt = Ks[buf];
+    const bf16_t* Vt = Vs[buf];
+    const bool diag = k0 + BK - 1 > qw;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 sacc = f32x16{}, pacc = f32x16{};
 #pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk) {
-          sacc[kb] = mfma32(ld8(Ks + (kb * 32 + r32) * ST + 16 * kk + 8 * h), qreg[kk], sacc[kb]);
-          pacc[kb] = mfma32(ld8(Vs + (kb * 32 + r32) * ST + 16 * kk + 8 * h), doreg[kk], pacc[kb]);
-        }
-      const bool diag = k0 + BK - 1 > qw;
+      for (int kk = 0; kk < D / 16; ++kk) {
+        sacc = mfma32(tile_row8<D>(Kt, kb * 32 + r32, 16 * kk + 8 * h), qreg[kk], sacc);
+        pacc = mfma32(tile_row8<D>(Vt, kb * 32 + r32, 16 * kk + 8 * h), doreg[kk], pacc);
+      }
+      bf16x8 db[2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int64_t key = k0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-          float pv = __builtin_amdgcn_exp2f(sacc[kb][i] * sl2 - lse2);
-          if (diag && key > myq) pv = 0.0f;
-          sacc[kb][i] = pv * (pacc[kb][i] - dlt);  // dS^T
-        }
-      bf16x8 db[4];
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
+      for (int u = 0; u < 2; ++u) {
         float f[8];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) f[t] = sacc[s >> 1][8 * (s & 1) + t];
-        db[s] = pack8(f);
+        for (int t = 0; t < 8; ++t) {
+          const int i = 8 * u + t;
+          float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[i], sl2, -lse2));
+          if (diag && k0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3) > myq) pv = 0.0f;
+          f[t] = pv * (pacc[i] - dlt);
+        }
+        db[u] = cvt8(f);
       }
 #pragma unroll
-      for (int d = 0; d < D / 32; ++d)
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
-          dqacc[d] = mfma32(tr_operand(Ks, ST, 16 * s, 32 * d, lane), db[s], dqacc[d]);
+        for (int d = 0; d < D / 32; ++d)
+          dqacc[d] = mfma32(tile_tr8<D>(Kt, kb * 32 + 16 * u, 32 * d, lane), db[u], dqacc[d]);
     }
-    __syncthreads();
   }
   if (myq < S) {
     bf16_t* o = dQ + bh * S * D + myq * D;
@@ -313,101 +361,113 @@ __global__ void __launch_bounds__(256) sdpa_bwd_dq_bf16(const bf16_t* __restrict
 }
 
 // ------------------------------------------------------------------ bf16 backward: dK, dV
-constexpr int CK = 128;  // keys per workgroup (4 waves x 32)
-constexpr int CQ = 64;   // queries per tile
+// Each wave owns 32 keys (their V rows stay in registers; the workgroup's K rows sit in LDS for
+// the whole kernel) and streams double-buffered Q/dO tiles with their lse and Delta:
+// S = Q K^T and dP = dO V^T (per lane: one key, 16 queries), then dV += P^T dO and
+// dK += dS^T Q with the transposed dO/Q operands read from the same LDS tiles. Query tiles are
+// processed in two 32-row halves to bound live registers.
+constexpr int KWV = 4;        // waves per workgroup (dK/dV)
+constexpr int CK = 32 * KWV;  // keys per workgroup
+constexpr int CQ = 64;        // queries per tile
 
 template <int D>
-__global__ void __launch_bounds__(256) sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K,
-                                                          const bf16_t* __restrict__ V, const bf16_t* __restrict__ dO,
-                                                          const float* __restrict__ LSE, const float* __restrict__ DELTA,
-                                                          bf16_t* __restrict__ dK, bf16_t* __restrict__ dV, int64_t S,
-                                                          float sl2, float scale) {
-  constexpr int ST = D + 8;
-  __shared__ __align__(16) bf16_t Qs[CQ * ST];
-  __shared__ __align__(16) bf16_t dOs[CQ * ST];
-  __shared__ float lse_s[CQ];
-  __shared__ float dlt_s[CQ];
+__global__ void __launch_bounds__(64 * KWV) __attribute__((amdgpu_waves_per_eu(1, 1)))
+sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
+                   const bf16_t* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ DELTA,
+                   bf16_t* __restrict__ dK, bf16_t* __restrict__ dV, int64_t S, float sl2, float scale) {
+  __shared__ __align__(16) bf16_t Qs[2][CQ * D];
+  __shared__ __align__(16) bf16_t dOs[2][CQ * D];
+  __shared__ __align__(16) float lse_s[2][CQ];
+  __shared__ __align__(16) float dlt_s[2][CQ];
+  __shared__ __align__(16) bf16_t Kw[CK * D];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int h = lane >> 5, r32 = lane & 31;
   const int64_t bh = blockIdx.y;
-  const int64_t k0 = (int64_t)blockIdx.x * CK;  // short key tiles (late keys) do little work
+  const int64_t k0 = (int64_t)blockIdx.x * CK;  // early keys see the most queries: launched first
   const int64_t kw = k0 + 32 * w;
   const int64_t mykey = kw + r32;
   const bf16_t* Qh = Q + bh * S * D;
   const bf16_t* Kh = K + bh * S * D;
   const bf16_t* Vh = V + bh * S * D;
   const bf16_t* dOh = dO + bh * S * D;
+  const float* Lh = LSE + bh * S;
+  const float* Dh = DELTA + bh * S;
 
-  bf16x8 kreg[D / 16], vreg[D / 16];
-#pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
-    if (mykey < S) {
-      kreg[kk] = ld8(Kh + mykey * D + 16 * kk + 8 * h);
-      vreg[kk] = ld8(Vh + mykey * D + 16 * kk + 8 * h);
-    } else {
-      kreg[kk] = bf16x8{};
-      vreg[kk] = bf16x8{};
+  const int64_t qstart = (k0 / CQ) * CQ;
+  const int nqt = (int)((S - qstart + CQ - 1) / CQ);
+  auto stage = [&](int b, int64_t qt0) {
+    load_tile_lds<D, CQ, KWV>(Qs[b], Qh, qt0, S, w, lane);
+    load_tile_lds<D, CQ, KWV>(dOs[b], dOh, qt0, S, w, lane);
+    if (tid < CQ) {
+      const int64_t q = qt0 + tid;
+      lse_s[b][tid] = q < S ? Lh[q] * kLog2e : INFINITY;
+      dlt_s[b][tid] = q < S ? Dh[q] : 0.0f;
     }
-  }
+  };
+  load_tile_lds<D, CK, KWV>(Kw, Kh, k0, S, w, lane);
+  stage(0, qstart);
+
+  const int64_t krow = mykey < S ? mykey : S - 1;
+  bf16x8 vreg[D / 16];
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) vreg[kk] = ld8(Vh + krow * D + 16 * kk + 8 * h);
   f32x16 dkacc[D / 32], dvacc[D / 32];
 #pragma unroll
   for (int d = 0; d < D / 32; ++d) dkacc[d] = dvacc[d] = f32x16{};
 
-  const int64_t qstart = (k0 / CQ) * CQ;
-  for (int64_t qt0 = qstart; qt0 < S; qt0 += CQ) {
-    for (int c = tid; c < CQ * (D / 8); c += 256) {
-      const int r = c / (D / 8), cc = c % (D / 8);
-      const int64_t q = qt0 + r;
-      u32x4 qv{0, 0, 0, 0}, dv{0, 0, 0, 0};
-      if (q < S) {
-        qv = *reinterpret_cast<const u32x4*>(Qh + q * D + cc * 8);
-        dv = *reinterpret_cast<const u32x4*>(dOh + q * D + cc * 8);
-      }
-      *reinterpret_cast<u32x4*>(Qs + r * ST + cc * 8) = qv;
-      *reinterpret_cast<u32x4*>(dOs + r * ST + cc * 8) = dv;
-    }
-    for (int c = tid; c < CQ; c += 256) {
-      const int64_t q = qt0 + c;
-      lse_s[c] = q < S ? LSE[bh * S + q] * kLog2e : INFINITY;
-      dlt_s[c] = q < S ? DELTA[bh * S + q] : 0.0f;
-    }
+  for (int it = 0; it < nqt; ++it) {
+    const int buf = it & 1;
+    const int64_t qt0 = qstart + (int64_t)it * CQ;
     __syncthreads();
-    if (qt0 + CQ - 1 >= kw && kw < S) {
-      f32x16 sacc[2] = {f32x16{}, f32x16{}}, pacc[2] = {f32x16{}, f32x16{}};
+    if (it + 1 < nqt) stage(buf ^ 1, qt0 + CQ);
+    if (qt0 + CQ - 1 < kw || kw >= S) continue;  // every query of the tile precedes this wave's keys
+    const bf16_t* Qt = Qs[buf];
+    const bf16_t* dOt = dOs[buf];
+    const bool diag = qt0 < kw + 31;
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
+    for (int qb = 0; qb < 2; ++qb) {
+      f32x16 sacc = f32x16{}, pacc = f32x16{};
 #pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk) {
-          sacc[qb] = mfma32(ld8(Qs + (qb * 32 + r32) * ST + 16 * kk + 8 * h), kreg[kk], sacc[qb]);
-          pacc[qb] = mfma32(ld8(dOs + (qb * 32 + r32) * ST + 16 * kk + 8 * h), vreg[kk], pacc[qb]);
-        }
-      const bool diag = qt0 < kw + 31;
-      bf16x8 pb[4], db[4];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        float pf[16], df[16];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int ql = qb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-          float pv = __builtin_amdgcn_exp2f(sacc[qb][i] * sl2 - lse_s[ql]);
-          if (diag && mykey > qt0 + ql) pv = 0.0f;
-          pf[i] = pv;
-          df[i] = pv * (pacc[qb][i] - dlt_s[ql]);
-        }
-        pb[2 * qb] = pack8(pf);
-        pb[2 * qb + 1] = pack8(pf + 8);
-        db[2 * qb] = pack8(df);
-        db[2 * qb + 1] = pack8(df + 8);
+      for (int kk = 0; kk < D / 16; ++kk) {
+        sacc = mfma32(tile_row8<D>(Qt, qb * 32 + r32, 16 * kk + 8 * h),
+                      tile_row8<D>(Kw, 32 * w + r32, 16 * kk + 8 * h), sacc);
+        pacc = mfma32(tile_row8<D>(dOt, qb * 32 + r32, 16 * kk + 8 * h), vreg[kk], pacc);
+        if (kk % 4 == 3) __builtin_amdgcn_sched_barrier(0);  // bound the operand loads in flight
       }
+      bf16x8 pb[2], db[2];
 #pragma unroll
-      for (int d = 0; d < D / 32; ++d)
+      for (int u = 0; u < 2; ++u) {
+        float pf[8], df[8];
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          dvacc[d] = mfma32(pb[s], tr_operand(dOs, ST, 16 * s, 32 * d, lane), dvacc[d]);
-          dkacc[d] = mfma32(db[s], tr_operand(Qs, ST, 16 * s, 32 * d, lane), dkacc[d]);
+        for (int g = 0; g < 2; ++g) {
+          const int qg = qb * 32 + 16 * u + 8 * g + 4 * h;  // rows qg .. qg + 3 in the tile
+          const float4 l4 = *reinterpret_cast<const float4*>(&lse_s[buf][qg]);
+          const float4 d4 = *reinterpret_cast<const float4*>(&dlt_s[buf][qg]);
+          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+          const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int i = 8 * u + 4 * g + j;
+            float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[i], sl2, -lv[j]));
+            if (diag && mykey > qt0 + qg + j) pv = 0.0f;
+            pf[4 * g + j] = pv;
+            df[4 * g + j] = pv * (pacc[i] - dv4[j]);
+          }
         }
+        pb[u] = cvt8(pf);
+        db[u] = cvt8(df);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // keep the operand loads of each phase together
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+#pragma unroll
+        for (int d = 0; d < D / 32; ++d) {
+          dvacc[d] = mfma32(pb[u], tile_tr8<D>(dOt, qb * 32 + 16 * u, 32 * d, lane), dvacc[d]);
+          dkacc[d] = mfma32(db[u], tile_tr8<D>(Qt, qb * 32 + 16 * u, 32 * d, lane), dkacc[d]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
-    __syncthreads();
   }
   // C layout: row = key kw + 8(i/4) + 4h + i%4, column d = 32 dblk + lane % 32
 #pragma unroll
@@ -586,8 +646,8 @@ hipError_t lh_launch_sdpa_fwd(const LhShape& s, const void* qs, const void* ks, 
     auto q = (const bf16_t*)qs;
     auto k = (const bf16_t*)ks;
     auto v = (const bf16_t*)vs;
-    if (s.D == 128) hipLaunchKernelGGL(sdpa_fwd_bf16<128>, grid, dim3(256), 0, st, q, k, v, (bf16_t*)os, lse, s.S, sl2);
-    else hipLaunchKernelGGL(sdpa_fwd_bf16<64>, grid, dim3(256), 0, st, q, k, v, (bf16_t*)os, lse, s.S, sl2);
+    if (s.D == 128) hipLaunchKernelGGL(sdpa_fwd_bf16<128>, grid, dim3(64 * FW), 0, st, q, k, v, (bf16_t*)os, lse, s.S, sl2);
+    else hipLaunchKernelGGL(sdpa_fwd_bf16<64>, grid, dim3(64 * FW), 0, st, q, k, v, (bf16_t*)os, lse, s.S, sl2);
   } else {
     dim3 grid((unsigned)((s.S + RT - 1) / RT), (unsigned)BH);
     auto q = (const float*)qs;
@@ -622,11 +682,11 @@ hipError_t lh_launch_sdpa_bwd(const LhShape& s, const void* qs, const void* ks, 
     dim3 gk((unsigned)((s.S + CK - 1) / CK), (unsigned)BH);
     dim3 gq((unsigned)((s.S + BQ - 1) / BQ), (unsigned)BH);
     if (s.D == 128) {
-      hipLaunchKernelGGL(sdpa_bwd_dkdv_bf16<128>, gk, dim3(256), 0, st, q, k, v, g, lse, delta, (bf16_t*)dks, (bf16_t*)dvs, s.S, sl2, s.scale);
-      hipLaunchKernelGGL(sdpa_bwd_dq_bf16<128>, gq, dim3(256), 0, st, q, k, v, g, lse, delta, (bf16_t*)dqs, s.S, sl2, s.scale);
+      hipLaunchKernelGGL(sdpa_bwd_dkdv_bf16<128>, gk, dim3(64 * KWV), 0, st, q, k, v, g, lse, delta, (bf16_t*)dks, (bf16_t*)dvs, s.S, sl2, s.scale);
+      hipLaunchKernelGGL(sdpa_bwd_dq_bf16<128>, gq, dim3(64 * QW), 0, st, q, k, v, g, lse, delta, (bf16_t*)dqs, s.S, sl2, s.scale);
     } else {
-      hipLaunchKernelGGL(sdpa_bwd_dkdv_bf16<64>, gk, dim3(256), 0, st, q, k, v, g, lse, delta, (bf16_t*)dks, (bf16_t*)dvs, s.S, sl2, s.scale);
-      hipLaunchKernelGGL(sdpa_bwd_dq_bf16<64>, gq, dim3(256), 0, st, q, k, v, g, lse, delta, (bf16_t*)dqs, s.S, sl2, s.scale);
+      hipLaunchKernelGGL(sdpa_bwd_dkdv_bf16<64>, gk, dim3(64 * KWV), 0, st, q, k, v, g, lse, delta, (bf16_t*)dks, (bf16_t*)dvs, s.S, sl2, s.scale);
+      hipLaunchKernelGGL(sdpa_bwd_dq_bf16<64>, gq, dim3(64 * QW), 0, st, q, k, v, g, lse, delta, (bf16_t*)dqs, s.S, sl2, s.scale);
     }
   } else {
     auto q = (const float*)qs;
