@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "liblighthouse.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["api.cpp", "k_pool_score.hip", "k_select.hip", "k_gather_scatter.hip", "k_sdpa.hip"]
+SOURCES = ["api.cpp", "k_pool_score.hip", "k_select.hip", "k_gather_scatter.hip", "k_sdpa.hip", "k_sdpa_mfma.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          # never emit packed fp32 ALU ops (v_pk_*_f32)
