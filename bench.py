@@ -116,8 +116,7 @@ def run_gpu(args, cfg):
     wsd = lh.workspace(pr, lh.LH_OP_SDPA_BWD, dev)
     dos, dqs, dks, dvs = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(4))
     stages = {
-        "pool_score": lambda: (lh.lh_pyramid_pool(pr, q, k, v, qp, kp, vp, stream=stream),
-                               lh.lh_score(pr, q, k, sqk, skq, stream=stream)),
+        "pool_score": lambda: lh.lh_pool_score(pr, q, k, v, qp, kp, vp, sqk, skq, stream=stream),
         "select": lambda: lh.lh_select_topk(pr, sqk, skq, idx, slot, wss, stream=stream),
         "gather": lambda: lh.lh_gather(pr, q, k, v, qp, kp, vp, idx, qs, ks, vs, stream=stream),
         "sdpa_fwd": lambda: lh.lh_sdpa_fwd(pr, qs, ks, vs, os_, lse, stream=stream),

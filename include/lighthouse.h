@@ -145,6 +145,11 @@ lh_status lh_pyramid_pool(const lh_problem* pr, const void* q, const void* k, co
 lh_status lh_score(const lh_problem* pr, const void* q, const void* k,
                    float* s_qk, float* s_kq, void* stream);
 
+/* lh_pyramid_pool and lh_score in one streaming pass over Q, K, V (each input row is read
+   once). Writes qpyr, kpyr, vpyr (when L > 1), s_qk and s_kq exactly as the two calls do. */
+lh_status lh_pool_score(const lh_problem* pr, const void* q, const void* k, const void* v,
+                        void* qpyr, void* kpyr, void* vpyr, float* s_qk, float* s_kq, void* stream);
+
 /* Sec. 3.4 (Eq. topk, Fig. 2 panel 3) and Sec. 3.5 (causal order): per (b, hq), the
    per-level descent described at the top of this file, then the causal ordering.
    Writes idx [B,Hq,S] and slot [B,Hq,Ptot] (-1 for entries not gathered).

@@ -18,8 +18,9 @@ __all__ = [
     "LH_OP_ATTENTION_FWD", "LH_OP_ATTENTION_BWD", "LighthouseError", "lh_problem", "problem",
     "lh_check", "lh_level_rows", "lh_level_offset", "lh_pyramid_rows", "lh_subseq_len",
     "lh_workspace_bytes", "lh_status_str", "lh_last_error", "lh_pyramid_pool", "lh_score",
-    "lh_select_topk", "lh_gather", "lh_sdpa_fwd", "lh_sdpa_bwd", "lh_scatter", "lh_scatter_bwd",
-    "lh_gather_bwd", "lh_attention_fwd", "lh_attention_bwd", "workspace", "attention_forward",
+    "lh_pool_score", "lh_select_topk", "lh_gather", "lh_sdpa_fwd", "lh_sdpa_bwd", "lh_scatter",
+    "lh_scatter_bwd", "lh_gather_bwd", "lh_attention_fwd", "lh_attention_bwd", "workspace",
+    "attention_forward",
     "attention_backward", "library_path", "EXPORTED",
 ]
 
@@ -34,7 +35,7 @@ library_path = os.path.join(_HERE, "liblighthouse.so")
 EXPORTED = [
     "lh_check", "lh_level_rows", "lh_level_offset", "lh_pyramid_rows", "lh_subseq_len",
     "lh_workspace_bytes", "lh_status_str", "lh_last_error", "lh_pyramid_pool", "lh_score",
-    "lh_select_topk", "lh_gather", "lh_sdpa_fwd", "lh_sdpa_bwd", "lh_scatter", "lh_scatter_bwd",
+    "lh_pool_score", "lh_select_topk", "lh_gather", "lh_sdpa_fwd", "lh_sdpa_bwd", "lh_scatter", "lh_scatter_bwd",
     "lh_gather_bwd", "lh_attention_fwd", "lh_attention_bwd",
 ]
 
@@ -85,6 +86,7 @@ def _load():
         "lh_last_error": (ctypes.c_char_p, []),
         "lh_pyramid_pool": (i32, [PR, P, P, P, P, P, P, P]),
         "lh_score": (i32, [PR, P, P, P, P, P]),
+        "lh_pool_score": (i32, [PR, P, P, P, P, P, P, P, P, P]),
         "lh_select_topk": (i32, [PR, P, P, P, P, P, sz, P]),
         "lh_gather": (i32, [PR, P, P, P, P, P, P, P, P, P, P, P]),
         "lh_sdpa_fwd": (i32, [PR, P, P, P, P, P, P]),
@@ -173,6 +175,11 @@ def lh_pyramid_pool(pr, q, k, v, qpyr, kpyr, vpyr, stream=None):
 
 def lh_score(pr, q, k, s_qk, s_kq, stream=None):
     _call("lh_score", ctypes.byref(pr), _p(q), _p(k), _p(s_qk), _p(s_kq), _stream(stream))
+
+
+def lh_pool_score(pr, q, k, v, qpyr, kpyr, vpyr, s_qk, s_kq, stream=None):
+    _call("lh_pool_score", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(qpyr), _p(kpyr), _p(vpyr), _p(s_qk),
+          _p(s_kq), _stream(stream))
 
 
 def lh_select_topk(pr, s_qk, s_kq, idx, slot, ws, ws_bytes=None, stream=None):

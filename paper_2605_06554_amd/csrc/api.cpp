@@ -250,6 +250,25 @@ lh_status lh_score(const lh_problem* pr, const void* q, const void* k, float* s_
                     "lh_score");
 }
 
+lh_status lh_pool_score(const lh_problem* pr, const void* q, const void* k, const void* v, void* qpyr,
+                        void* kpyr, void* vpyr, float* s_qk, float* s_kq, void* stream) {
+  LhShape s;
+  LH_TRY(make_shape(pr, &s));
+  LH_TRY(need_ptr(q, "q"));
+  LH_TRY(need_ptr(k, "k"));
+  LH_TRY(need_ptr(v, "v"));
+  if (s.L > 1) {
+    LH_TRY(need_ptr(qpyr, "qpyr"));
+    LH_TRY(need_ptr(kpyr, "kpyr"));
+    LH_TRY(need_ptr(vpyr, "vpyr"));
+  }
+  LH_TRY(need_ptr(s_qk, "s_qk"));
+  LH_TRY(need_ptr(s_kq, "s_kq"));
+  g_err[0] = 0;
+  return hip_status(lh_launch_pool_score(s, q, k, v, qpyr, kpyr, vpyr, s_qk, s_kq, (hipStream_t)stream),
+                    "lh_pool_score");
+}
+
 lh_status lh_select_topk(const lh_problem* pr, const float* s_qk, const float* s_kq, int32_t* idx,
                          int32_t* slot, void* ws, size_t ws_bytes_, void* stream) {
   LhShape s;

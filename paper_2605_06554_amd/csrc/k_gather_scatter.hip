@@ -72,8 +72,9 @@ struct ScatterArgs {
 };
 
 // o[b, j, hq, :]: consecutive threads cover consecutive (hq, chunk) of one base row, so the
-// [B, N, Hq, D] output is written contiguously.
-template <typename T>
+// [B, N, Hq, D] output is written contiguously. The L slot lookups are issued together, then
+// the L row loads, so a thread waits for two memory latencies rather than 2 L.
+template <typename T, int L>
 __global__ void __launch_bounds__(256) scatter_kernel(ScatterArgs a) {
   constexpr int CH = 16 / sizeof(T);
   const int CPR = a.D / CH;
@@ -87,19 +88,28 @@ __global__ void __launch_bounds__(256) scatter_kernel(ScatterArgs a) {
   const int64_t bh = b * a.Hq + hq;
   const int32_t* sl = a.slot + bh * a.Ptot;
   const T* src = reinterpret_cast<const T*>(a.os) + bh * a.S * a.D + cc * CH;
+  int32_t m[L];
+#pragma unroll
+  for (int l = L - 1; l >= 0; --l) {
+    const int64_t i = (j + 1) / a.pw[l] - 1;
+    m[l] = i < 0 ? -1 : sl[a.off[l] + i];
+  }
+  float v[L][CH];
+#pragma unroll
+  for (int l = L - 1; l >= 0; --l) {
+    if (m[l] >= 0 && m[l] < a.S) load_chunk<T>(src + (int64_t)m[l] * a.D, v[l]);
+    else {
+#pragma unroll
+      for (int c = 0; c < CH; ++c) v[l][c] = 0.0f;
+    }
+  }
   float acc[CH];
 #pragma unroll
   for (int c = 0; c < CH; ++c) acc[c] = 0.0f;
-  for (int l = a.L - 1; l >= 0; --l) {
-    const int64_t i = (j + 1) / a.pw[l] - 1;
-    if (i < 0) continue;
-    const int32_t m = sl[a.off[l] + i];
-    if (m < 0 || m >= a.S) continue;
-    float v[CH];
-    load_chunk<T>(src + (int64_t)m * a.D, v);
 #pragma unroll
-    for (int c = 0; c < CH; ++c) acc[c] += v[c];
-  }
+  for (int l = L - 1; l >= 0; --l)
+#pragma unroll
+    for (int c = 0; c < CH; ++c) acc[c] += v[l][c];
   store_chunk<T>(reinterpret_cast<T*>(a.o) + ((b * a.N + j) * a.Hq + hq) * a.D + cc * CH, acc);
 }
 
@@ -195,7 +205,31 @@ struct GatherBwdArgs {
   float inv[16];
 };
 
-template <typename T>
+// Output head h sums query heads h Gs .. h Gs + Gs - 1 (Gs = G for dK/dV, 1 for dQ) over the
+// levels, in the order (query head ascending, level L-1 first). For each query head the L slot
+// lookups are issued together, then the L row loads; with GS > 0 (compile-time group size) the
+// lookups of all heads go out first.
+template <typename T, int L>
+__device__ __forceinline__ void gather_bwd_head(const GatherBwdArgs& a, const int32_t* m, int64_t bhq, int cc,
+                                                float* acc) {
+  constexpr int CH = 16 / sizeof(T);
+  const T* src = reinterpret_cast<const T*>(a.src) + bhq * a.S * a.D + cc * CH;
+  float v[L][CH];
+#pragma unroll
+  for (int l = L - 1; l >= 0; --l) {
+    if (m[l] >= 0 && m[l] < a.S) load_chunk<T>(src + (int64_t)m[l] * a.D, v[l]);
+    else {
+#pragma unroll
+      for (int c = 0; c < CH; ++c) v[l][c] = 0.0f;
+    }
+  }
+#pragma unroll
+  for (int l = L - 1; l >= 0; --l)
+#pragma unroll
+    for (int c = 0; c < CH; ++c) acc[c] += v[l][c] * a.inv[l];
+}
+
+template <typename T, int L, int GS>
 __global__ void __launch_bounds__(256) gather_bwd_kernel(GatherBwdArgs a) {
   constexpr int CH = 16 / sizeof(T);
   const int CPR = a.D / CH;
@@ -209,20 +243,66 @@ __global__ void __launch_bounds__(256) gather_bwd_kernel(GatherBwdArgs a) {
   float acc[CH];
 #pragma unroll
   for (int c = 0; c < CH; ++c) acc[c] = 0.0f;
-  for (int gq = 0; gq < a.Gs; ++gq) {
-    const int64_t bh = b * a.Hq + (int64_t)h * a.Gs + gq;
-    const int32_t* sl = a.slot + bh * a.Ptot;
-    const T* src = reinterpret_cast<const T*>(a.src) + bh * a.S * a.D + cc * CH;
-    for (int l = a.L - 1; l >= 0; --l) {
-      const int32_t m = sl[a.off[l] + j / a.pw[l]];
-      if (m < 0 || m >= a.S) continue;
-      float v[CH];
-      load_chunk<T>(src + (int64_t)m * a.D, v);
+  if constexpr (GS > 0) {
+    int32_t m[GS][L];
 #pragma unroll
-      for (int c = 0; c < CH; ++c) acc[c] += v[c] * a.inv[l];
+    for (int g = 0; g < GS; ++g) {
+      const int32_t* sl = a.slot + (b * a.Hq + (int64_t)h * GS + g) * a.Ptot;
+#pragma unroll
+      for (int l = L - 1; l >= 0; --l) m[g][l] = sl[a.off[l] + j / a.pw[l]];
+    }
+#pragma unroll
+    for (int g = 0; g < GS; ++g) gather_bwd_head<T, L>(a, m[g], b * a.Hq + (int64_t)h * GS + g, cc, acc);
+  } else {
+    for (int g = 0; g < a.Gs; ++g) {
+      const int64_t bhq = b * a.Hq + (int64_t)h * a.Gs + g;
+      const int32_t* sl = a.slot + bhq * a.Ptot;
+      int32_t m[L];
+#pragma unroll
+      for (int l = L - 1; l >= 0; --l) m[l] = sl[a.off[l] + j / a.pw[l]];
+      gather_bwd_head<T, L>(a, m, bhq, cc, acc);
     }
   }
   store_chunk<T>(reinterpret_cast<T*>(a.dst) + ((b * a.N + j) * a.H + h) * a.D + cc * CH, acc);
+}
+
+template <typename T, int L>
+static void launch_gather_bwd_G(const GatherBwdArgs& a, dim3 grid, hipStream_t st) {
+  switch (a.Gs) {
+    case 1: hipLaunchKernelGGL((gather_bwd_kernel<T, L, 1>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((gather_bwd_kernel<T, L, 2>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((gather_bwd_kernel<T, L, 4>), grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((gather_bwd_kernel<T, L, 8>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((gather_bwd_kernel<T, L, 0>), grid, dim3(256), 0, st, a); break;
+  }
+}
+
+template <typename T>
+static void launch_gather_bwd_L(const GatherBwdArgs& a, dim3 grid, hipStream_t st) {
+  switch (a.L) {
+    case 1: launch_gather_bwd_G<T, 1>(a, grid, st); break;
+    case 2: launch_gather_bwd_G<T, 2>(a, grid, st); break;
+    case 3: launch_gather_bwd_G<T, 3>(a, grid, st); break;
+    case 4: launch_gather_bwd_G<T, 4>(a, grid, st); break;
+    case 5: launch_gather_bwd_G<T, 5>(a, grid, st); break;
+    case 6: launch_gather_bwd_G<T, 6>(a, grid, st); break;
+    case 7: launch_gather_bwd_G<T, 7>(a, grid, st); break;
+    default: launch_gather_bwd_G<T, 8>(a, grid, st); break;
+  }
+}
+
+template <typename T>
+static void launch_scatter_L(const ScatterArgs& a, dim3 grid, hipStream_t st) {
+  switch (a.L) {
+    case 1: hipLaunchKernelGGL((scatter_kernel<T, 1>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((scatter_kernel<T, 2>), grid, dim3(256), 0, st, a); break;
+    case 3: hipLaunchKernelGGL((scatter_kernel<T, 3>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((scatter_kernel<T, 4>), grid, dim3(256), 0, st, a); break;
+    case 5: hipLaunchKernelGGL((scatter_kernel<T, 5>), grid, dim3(256), 0, st, a); break;
+    case 6: hipLaunchKernelGGL((scatter_kernel<T, 6>), grid, dim3(256), 0, st, a); break;
+    case 7: hipLaunchKernelGGL((scatter_kernel<T, 7>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((scatter_kernel<T, 8>), grid, dim3(256), 0, st, a); break;
+  }
 }
 
 template <typename T, int L>
@@ -297,8 +377,8 @@ hipError_t lh_launch_scatter(const LhShape& s, const void* os, const int32_t* sl
   const int CH = s.dtype == LH_BF16 ? 8 : 4;
   const int64_t n = s.N * s.Hq * (s.D / CH);
   dim3 grid((unsigned)((n + 255) / 256), (unsigned)s.B);
-  if (s.dtype == LH_BF16) hipLaunchKernelGGL(scatter_kernel<bf16_t>, grid, dim3(256), 0, st, a);
-  else hipLaunchKernelGGL(scatter_kernel<float>, grid, dim3(256), 0, st, a);
+  if (s.dtype == LH_BF16) launch_scatter_L<bf16_t>(a, grid, st);
+  else launch_scatter_L<float>(a, grid, st);
   return hipGetLastError();
 }
 
@@ -334,8 +414,8 @@ hipError_t lh_launch_gather_bwd(const LhShape& s, const void* dqs, const void* d
     const int CH = s.dtype == LH_BF16 ? 8 : 4;
     const int64_t n = s.N * a.H * (s.D / CH);
     dim3 grid((unsigned)((n + 255) / 256), (unsigned)s.B);
-    if (s.dtype == LH_BF16) hipLaunchKernelGGL(gather_bwd_kernel<bf16_t>, grid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL(gather_bwd_kernel<float>, grid, dim3(256), 0, st, a);
+    if (s.dtype == LH_BF16) launch_gather_bwd_L<bf16_t>(a, grid, st);
+    else launch_gather_bwd_L<float>(a, grid, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

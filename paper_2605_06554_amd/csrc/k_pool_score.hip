@@ -25,6 +25,8 @@ struct PoolArgs {
   int32_t H, D, HW;
   int64_t pw[16];
   int64_t off[17];
+  double inv[16];  // 1 / p^l, used only when it is exact (p a power of two)
+  int32_t pow2;
 };
 
 template <typename T, int L>
@@ -93,21 +95,23 @@ __global__ void __launch_bounds__(1024) pool_score_kernel(PoolArgs a) {
           for (int l = 1; l < L; ++l) {
             if ((j + 1) % a.pw[l] != 0) break;
             const int64_t i = (j + 1) / a.pw[l] - 1;
-            const double inv = (double)a.pw[l];
+            const double w = (double)a.pw[l], inv = a.inv[l];
+            // mean = sum / p^l, rounded once; the reciprocal is exact when p is a power of two
+            auto mean = [&](double x) { return a.pow2 ? x * inv : x / w; };
             T* dst = pyr + ((b * a.R + (a.off[l] - a.N) + i) * a.H + h) * D + cc * CH;
             if constexpr (sizeof(T) == 2) {
-              uint32_t w[4];
+              uint32_t wd[4];
 #pragma unroll
               for (int c = 0; c < 4; ++c)
-                w[c] = (uint32_t)f64_to_bf16(acc[l][2 * c] / inv) |
-                       ((uint32_t)f64_to_bf16(acc[l][2 * c + 1] / inv) << 16);
+                wd[c] = (uint32_t)f64_to_bf16(mean(acc[l][2 * c])) |
+                       ((uint32_t)f64_to_bf16(mean(acc[l][2 * c + 1])) << 16);
               u32x4 o;
-              o.x = w[0], o.y = w[1], o.z = w[2], o.w = w[3];
+              o.x = wd[0], o.y = wd[1], o.z = wd[2], o.w = wd[3];
               *reinterpret_cast<u32x4*>(dst) = o;
             } else {
               float o[CH];
 #pragma unroll
-              for (int c = 0; c < CH; ++c) o[c] = (float)(acc[l][c] / inv);
+              for (int c = 0; c < CH; ++c) o[c] = (float)mean(acc[l][c]);
               store_chunk_f32(reinterpret_cast<float*>(dst), o);
             }
             if (l + 1 < L) {
@@ -182,7 +186,11 @@ static hipError_t launch_one(const LhShape& s, const void* x, void* pyr, float* 
   if (a.HW < 1) a.HW = 1;
   int64_t P = s.P;
   a.WR = P >= 64 ? P : P * ((64 + P - 1) / P);
-  for (int l = 0; l < 16; ++l) a.pw[l] = s.pw[l];
+  for (int l = 0; l < 16; ++l) {
+    a.pw[l] = s.pw[l];
+    a.inv[l] = l < s.L ? 1.0 / (double)s.pw[l] : 0.0;
+  }
+  a.pow2 = (s.p & (s.p - 1)) == 0;
   for (int l = 0; l < 17; ++l) a.off[l] = s.off[l];
   dim3 grid((unsigned)((s.N + a.WR - 1) / a.WR), (unsigned)((H + a.HW - 1) / a.HW), (unsigned)s.B);
   dim3 block((unsigned)(a.HW * CPR));

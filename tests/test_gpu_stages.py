@@ -53,7 +53,13 @@ def test_pool_and_score(name):
     skq = torch.empty(c.B, c.Hkv, Ptot, dtype=torch.float32, device=DEV)
     lh.lh_pyramid_pool(pr, q, k, v, qp, kp, vp)
     lh.lh_score(pr, q, k, sqk, skq)
+    # the fused single pass must write exactly the same bytes
+    qp2, kp2, vp2, sqk2, skq2 = (torch.empty_like(t) for t in (qp, kp, vp, sqk, skq))
+    lh.lh_pool_score(pr, q, k, v, qp2, kp2, vp2, sqk2, skq2)
     torch.cuda.synchronize()
+    assert torch.equal(sqk, sqk2) and torch.equal(skq, skq2)
+    if R > 0:
+        assert torch.equal(qp, qp2) and torch.equal(kp, kp2) and torch.equal(vp, vp2)
     h = oracle.Head(c.N, c.D, c.p, c.L, c.k, _odt(c))
     for b in range(c.B):
         for hh in range(c.Hq):
