@@ -169,7 +169,7 @@ static int ord_cmp(const void* a, const void* b) {
   return x < y ? -1 : x > y ? 1 : 0;
 }
 
-/* Selection (Eq. topk with Fig. 2 panel 3, Sec. 3.4 "coarsest level retained in full") and
+/* Selection (Eq. topk with Fig. 2 panel 3; Sec. 3.4 keeps the whole coarsest level) and
    causal ordering (Sec. 3.5, mask paragraph). Reading of the selection: per-level descent.
      E_{L-1} = all entries of the coarsest level.
      For l = L-1 down to 1: rank E_l by (c desc, i asc) with c = max(s_QK, s_KQ) (an entry
