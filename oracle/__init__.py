@@ -66,6 +66,8 @@ def _load():
         "lho_select": (i64, [H, P, P, P, i64, P]),
         "lho_gather": (None, [H, P, P, i64, P]),
         "lho_sdpa_fwd": (None, [i64, ctypes.c_int, dbl, P, P, P, P, P, i64, i64]),
+        "lho_sdpa_fwd_rows": (None, [i64, ctypes.c_int, dbl, P, P, P, P, P, P, i64]),
+        "lho_sdpa_bwd_dq_rows": (None, [i64, ctypes.c_int, dbl, P, P, P, P, P, P, P, P, i64]),
         "lho_sdpa_bwd": (None, [i64, ctypes.c_int, dbl, P, P, P, P, P, P, P, P, P,
                                 i64, i64, i64, i64]),
         "lho_scatter": (None, [H, P, i64, P, P, i64]),
@@ -159,15 +161,22 @@ def gather(h: Head, pyr: np.ndarray, idx: np.ndarray) -> np.ndarray:
     return out
 
 
-def sdpa_fwd(qs, ks, vs, scale: float, rows=None):
+def sdpa_fwd(qs, ks, vs, scale: float, rows=None, row_list=None):
     """Causal SDPA over the gathered order (Eqs. sdpa, attn-sub). Returns (os, lse); only rows
-    in ``rows = (r0, r1)`` are computed (others are left 0)."""
+    in ``rows = (r0, r1)`` and, if given, the rows listed in ``row_list`` are computed (others
+    are left 0). With only ``row_list`` given, only those rows are computed."""
     qs, ks, vs = (np.ascontiguousarray(a, np.float64) for a in (qs, ks, vs))
     S, D = qs.shape
-    r0, r1 = rows if rows is not None else (0, S)
     os_ = np.zeros((S, D), np.float64)
     lse = np.zeros(S, np.float64)
-    _load().lho_sdpa_fwd(S, D, scale, _ptr(qs), _ptr(ks), _ptr(vs), _ptr(os_), _ptr(lse), r0, r1)
+    if rows is not None or row_list is None:
+        r0, r1 = rows if rows is not None else (0, S)
+        _load().lho_sdpa_fwd(S, D, scale, _ptr(qs), _ptr(ks), _ptr(vs), _ptr(os_), _ptr(lse), r0, r1)
+    if row_list is not None:
+        rl = np.ascontiguousarray(row_list, np.int64)
+        assert rl.size == 0 or (rl.min() >= 0 and rl.max() < S)
+        _load().lho_sdpa_fwd_rows(S, D, scale, _ptr(qs), _ptr(ks), _ptr(vs), _ptr(os_), _ptr(lse),
+                                  _ptr(rl), rl.size)
     return os_, lse
 
 
@@ -183,6 +192,22 @@ def sdpa_bwd(qs, ks, vs, os_, lse, dos, scale: float, qrows=None, krows=None):
     _load().lho_sdpa_bwd(S, D, scale, _ptr(qs), _ptr(ks), _ptr(vs), _ptr(os_), _ptr(lse), _ptr(dos),
                          _ptr(dqs), _ptr(dks), _ptr(dvs), q0, q1, k0, k1)
     return dqs, dks, dvs
+
+
+def sdpa_bwd_dq_rows(qs, ks, vs, os_, lse, dos, scale: float, row_list, dqs=None):
+    """dq of sdpa_bwd for the listed rows only (os_ and lse exact for those rows), written
+    into dqs (a new zero array if None)."""
+    qs, ks, vs, os_, dos = (np.ascontiguousarray(a, np.float64) for a in (qs, ks, vs, os_, dos))
+    lse = np.ascontiguousarray(lse, np.float64)
+    S, D = qs.shape
+    if dqs is None:
+        dqs = np.zeros((S, D), np.float64)
+    assert dqs.shape == (S, D) and dqs.dtype == np.float64 and dqs.flags.c_contiguous
+    rl = np.ascontiguousarray(row_list, np.int64)
+    assert rl.size == 0 or (rl.min() >= 0 and rl.max() < S)
+    _load().lho_sdpa_bwd_dq_rows(S, D, scale, _ptr(qs), _ptr(ks), _ptr(vs), _ptr(os_), _ptr(lse), _ptr(dos),
+                                 _ptr(dqs), _ptr(rl), rl.size)
+    return dqs
 
 
 def scatter(h: Head, idx, os_) -> np.ndarray:

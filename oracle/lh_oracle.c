@@ -285,9 +285,29 @@ void lho_gather(const lho_head* h, const double* pyr, const int32_t* idx, int64_
 
 /* ---------------------------------------------------------------- SDPA (Eqs. sdpa, attn-sub) */
 
-/* Causal softmax attention over the gathered order (the mask is lower-triangular on it):
-   for rows m in [r0, r1): a_t = scale <q_m, k_t> for t <= m, mu = max a, Z = sum exp(a - mu),
-   os[m] = sum_t exp(a_t - mu) / Z v_t, lse[m] = mu + log Z. */
+/* Causal softmax attention over the gathered order (the mask is lower-triangular on it), for
+   one row m: a_t = scale <q_m, k_t> for t <= m, mu = max a, Z = sum exp(a - mu),
+   os[m] = sum_t exp(a_t - mu) / Z v_t, lse[m] = mu + log Z. `a` has room for m + 1 values. */
+static void sdpa_fwd_row(int D, double scale, const double* qs, const double* ks, const double* vs,
+                         double* os, double* lse, int64_t m, double* a) {
+  double mu = -INFINITY;
+  for (int64_t t = 0; t <= m; ++t) {
+    double d = 0.0;
+    for (int c = 0; c < D; ++c) d += qs[m * D + c] * ks[t * D + c];
+    a[t] = scale * d;
+    if (a[t] > mu) mu = a[t];
+  }
+  double Z = 0.0;
+  for (int64_t t = 0; t <= m; ++t) Z += exp(a[t] - mu);
+  for (int c = 0; c < D; ++c) os[m * D + c] = 0.0;
+  for (int64_t t = 0; t <= m; ++t) {
+    const double w = exp(a[t] - mu) / Z;
+    for (int c = 0; c < D; ++c) os[m * D + c] += w * vs[t * D + c];
+  }
+  lse[m] = mu + log(Z);
+}
+
+/* Rows m in [r0, r1) of the causal attention above. */
 void lho_sdpa_fwd(int64_t S, int D, double scale, const double* qs, const double* ks,
                   const double* vs, double* os, double* lse, int64_t r0, int64_t r1) {
   if (r1 > S) r1 = S;
@@ -295,23 +315,20 @@ void lho_sdpa_fwd(int64_t S, int D, double scale, const double* qs, const double
   {
     double* a = (double*)malloc(sizeof(double) * (size_t)(S > 0 ? S : 1));
 #pragma omp for schedule(dynamic, 4)
-    for (int64_t m = r0; m < r1; ++m) {
-      double mu = -INFINITY;
-      for (int64_t t = 0; t <= m; ++t) {
-        double d = 0.0;
-        for (int c = 0; c < D; ++c) d += qs[m * D + c] * ks[t * D + c];
-        a[t] = scale * d;
-        if (a[t] > mu) mu = a[t];
-      }
-      double Z = 0.0;
-      for (int64_t t = 0; t <= m; ++t) Z += exp(a[t] - mu);
-      for (int c = 0; c < D; ++c) os[m * D + c] = 0.0;
-      for (int64_t t = 0; t <= m; ++t) {
-        const double w = exp(a[t] - mu) / Z;
-        for (int c = 0; c < D; ++c) os[m * D + c] += w * vs[t * D + c];
-      }
-      lse[m] = mu + log(Z);
-    }
+    for (int64_t m = r0; m < r1; ++m) sdpa_fwd_row(D, scale, qs, ks, vs, os, lse, m, a);
+    free(a);
+  }
+}
+
+/* The listed rows rows[0..n) (each in [0, S)) of the causal attention above; other rows of os
+   and lse are not touched. Lets a test evaluate sampled rows of a long sequence. */
+void lho_sdpa_fwd_rows(int64_t S, int D, double scale, const double* qs, const double* ks,
+                       const double* vs, double* os, double* lse, const int64_t* rows, int64_t n) {
+#pragma omp parallel
+  {
+    double* a = (double*)malloc(sizeof(double) * (size_t)(S > 0 ? S : 1));
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t r = 0; r < n; ++r) sdpa_fwd_row(D, scale, qs, ks, vs, os, lse, rows[r], a);
     free(a);
   }
 }
@@ -319,57 +336,79 @@ void lho_sdpa_fwd(int64_t S, int D, double scale, const double* qs, const double
 /* Adjoint of lho_sdpa_fwd, written from the definition with P recomputed from lse:
    P_mt = exp(scale <q_m, k_t> - lse_m) for t <= m; Delta_m = <dO_m, O_m>;
    dS_mt = P_mt (<dO_m, v_t> - Delta_m);
-   dq_m = scale sum_{t<=m} dS_mt k_t      (rows m in [q0, q1))
-   dk_t = scale sum_{m>=t} dS_mt q_m, dv_t = sum_{m>=t} P_mt dO_m   (rows t in [k0, k1)).
-   The os and lse passed in must be the forward's for every row m >= k0 (and m in [q0,q1)). */
+   dq_m = scale sum_{t<=m} dS_mt k_t
+   dk_t = scale sum_{m>=t} dS_mt q_m, dv_t = sum_{m>=t} P_mt dO_m. */
+static double sdpa_delta_row(int D, const double* os, const double* dos, int64_t m) {
+  double d = 0.0;
+  for (int c = 0; c < D; ++c) d += dos[m * D + c] * os[m * D + c];
+  return d;
+}
+
+/* dq_m; needs os and lse of row m. */
+static void sdpa_dq_row(int D, double scale, const double* qs, const double* ks, const double* vs,
+                        const double* os, const double* lse, const double* dos, double* dqs, int64_t m) {
+  const double delta = sdpa_delta_row(D, os, dos, m);
+  for (int c = 0; c < D; ++c) dqs[m * D + c] = 0.0;
+  for (int64_t t = 0; t <= m; ++t) {
+    double a = 0.0, dp = 0.0;
+    for (int c = 0; c < D; ++c) {
+      a += qs[m * D + c] * ks[t * D + c];
+      dp += dos[m * D + c] * vs[t * D + c];
+    }
+    const double P = exp(scale * a - lse[m]);
+    const double dS = P * (dp - delta);
+    for (int c = 0; c < D; ++c) dqs[m * D + c] += scale * dS * ks[t * D + c];
+  }
+}
+
+/* dk_t and dv_t; needs os, lse and delta of every row m >= t. */
+static void sdpa_dkv_row(int64_t S, int D, double scale, const double* qs, const double* ks,
+                         const double* vs, const double* lse, const double* delta, const double* dos,
+                         double* dks, double* dvs, int64_t t) {
+  for (int c = 0; c < D; ++c) {
+    dks[t * D + c] = 0.0;
+    dvs[t * D + c] = 0.0;
+  }
+  for (int64_t m = t; m < S; ++m) {
+    double a = 0.0, dp = 0.0;
+    for (int c = 0; c < D; ++c) {
+      a += qs[m * D + c] * ks[t * D + c];
+      dp += dos[m * D + c] * vs[t * D + c];
+    }
+    const double P = exp(scale * a - lse[m]);
+    const double dS = P * (dp - delta[m]);
+    for (int c = 0; c < D; ++c) {
+      dks[t * D + c] += scale * dS * qs[m * D + c];
+      dvs[t * D + c] += P * dos[m * D + c];
+    }
+  }
+}
+
+/* dq for rows m in [q0, q1) and dk, dv for rows t in [k0, k1). The os and lse passed in must be
+   the forward's for every row m >= k0 and every m in [q0, q1). */
 void lho_sdpa_bwd(int64_t S, int D, double scale, const double* qs, const double* ks,
                   const double* vs, const double* os, const double* lse, const double* dos,
                   double* dqs, double* dks, double* dvs, int64_t q0, int64_t q1, int64_t k0,
                   int64_t k1) {
   if (q1 > S) q1 = S;
   if (k1 > S) k1 = S;
-  int64_t lo = q0 < k0 ? q0 : k0;
-  double* delta = (double*)malloc(sizeof(double) * (size_t)(S > 0 ? S : 1));
-  for (int64_t m = lo; m < S; ++m) {
-    double d = 0.0;
-    for (int c = 0; c < D; ++c) d += dos[m * D + c] * os[m * D + c];
-    delta[m] = d;
-  }
 #pragma omp parallel for schedule(dynamic, 4)
-  for (int64_t m = q0; m < q1; ++m) {
-    for (int c = 0; c < D; ++c) dqs[m * D + c] = 0.0;
-    for (int64_t t = 0; t <= m; ++t) {
-      double a = 0.0, dp = 0.0;
-      for (int c = 0; c < D; ++c) {
-        a += qs[m * D + c] * ks[t * D + c];
-        dp += dos[m * D + c] * vs[t * D + c];
-      }
-      const double P = exp(scale * a - lse[m]);
-      const double dS = P * (dp - delta[m]);
-      for (int c = 0; c < D; ++c) dqs[m * D + c] += scale * dS * ks[t * D + c];
-    }
-  }
+  for (int64_t m = q0; m < q1; ++m) sdpa_dq_row(D, scale, qs, ks, vs, os, lse, dos, dqs, m);
+  if (k0 >= k1) return;
+  double* delta = (double*)malloc(sizeof(double) * (size_t)S);
+  for (int64_t m = k0; m < S; ++m) delta[m] = sdpa_delta_row(D, os, dos, m);
 #pragma omp parallel for schedule(dynamic, 4)
-  for (int64_t t = k0; t < k1; ++t) {
-    for (int c = 0; c < D; ++c) {
-      dks[t * D + c] = 0.0;
-      dvs[t * D + c] = 0.0;
-    }
-    for (int64_t m = t; m < S; ++m) {
-      double a = 0.0, dp = 0.0;
-      for (int c = 0; c < D; ++c) {
-        a += qs[m * D + c] * ks[t * D + c];
-        dp += dos[m * D + c] * vs[t * D + c];
-      }
-      const double P = exp(scale * a - lse[m]);
-      const double dS = P * (dp - delta[m]);
-      for (int c = 0; c < D; ++c) {
-        dks[t * D + c] += scale * dS * qs[m * D + c];
-        dvs[t * D + c] += P * dos[m * D + c];
-      }
-    }
-  }
+  for (int64_t t = k0; t < k1; ++t) sdpa_dkv_row(S, D, scale, qs, ks, vs, lse, delta, dos, dks, dvs, t);
   free(delta);
+}
+
+/* dq for the listed rows rows[0..n) only (os and lse needed for those rows). */
+void lho_sdpa_bwd_dq_rows(int64_t S, int D, double scale, const double* qs, const double* ks,
+                          const double* vs, const double* os, const double* lse, const double* dos,
+                          double* dqs, const int64_t* rows, int64_t n) {
+  (void)S;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t r = 0; r < n; ++r) sdpa_dq_row(D, scale, qs, ks, vs, os, lse, dos, dqs, rows[r]);
 }
 
 /* ---------------------------------------------------------------- scatter (Sec. 3.6) */

@@ -8,27 +8,78 @@
 //                dk/dv also summed over the query heads of the KV group.
 //
 // All accumulate in fp32 in a fixed order and round once; every thread owns a 16-byte column
-// chunk so that rows are read and written with full 16-byte vector accesses.
+// chunk so that rows are read and written with full 16-byte vector accesses. Row and entry
+// indices are 32-bit (the library rejects pyramids of 2^31 entries or more); element offsets
+// are 64-bit.
+//
+// Runs (scatter, gather_bwd). A thread handles a run of p consecutive base positions. The run
+// is aligned to p and p^l is a multiple of p, so the level-l entry (l >= 1) is the same for the
+// whole run: its row is read once per run, and only level 0 is looked up per position. Run c
+// covers j = c p + r - 1 (scatter, whose ranges are shifted by one) or j = c p + r
+// (gather_bwd), r = 0..p-1, and its level-l entry index is floor(c / p^(l-1)), minus one for
+// the scatter.
+//
+// XCD-aware order. Workgroups go round-robin to the 8 XCDs, each with its own L2, in order of
+// their linear id. Neighbouring runs share their coarse rows, so the run index is remapped to
+// give every XCD one contiguous eighth of the runs.
 #include "lh_common.h"
 
 namespace lh {
+
+// With gridDim.x a multiple of 8, blockIdx.x % 8 is the XCD of the workgroup; XCD x gets the
+// x-th contiguous eighth of [0, nx).
+__device__ __forceinline__ uint32_t xcd_contiguous(uint32_t bx, uint32_t nx) {
+  return (bx & 7u) * (nx >> 3) + (bx >> 3);
+}
+
+template <typename T>
+__device__ __forceinline__ void add_chunk(float* acc, const u32x4& w) {
+  const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[2 * i] += __uint_as_float(u[i] << 16);
+      acc[2 * i + 1] += __uint_as_float(u[i] & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] += __uint_as_float(u[i]);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void add_chunk_scaled(float* acc, const u32x4& w, float s) {
+  const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[2 * i] += __uint_as_float(u[i] << 16) * s;
+      acc[2 * i + 1] += __uint_as_float(u[i] & 0xffff0000u) * s;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] += __uint_as_float(u[i]) * s;
+  }
+}
+
+__device__ __forceinline__ u32x4 load_raw(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// ---------------------------------------------------------------- gather
 
 struct GatherArgs {
   const void *q, *k, *v, *qp, *kp, *vp;
   const int32_t* idx;
   void *qs, *ks, *vs;
   int64_t N, R, S;
-  int32_t Hq, Hkv, G, D;
+  int32_t Hq, Hkv, G, D, cpr_shift, rows_per_block;
 };
 
 template <typename T>
 __global__ void __launch_bounds__(256) gather_kernel(GatherArgs a) {
   constexpr int CH = 16 / sizeof(T);
-  const int CPR = a.D / CH;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= a.S * CPR) return;
-  const int64_t m = t / CPR;
-  const int cc = (int)(t % CPR);
+  const int cc = threadIdx.x & ((1 << a.cpr_shift) - 1);
+  const int64_t m = (int64_t)blockIdx.x * a.rows_per_block + (threadIdx.x >> a.cpr_shift);
+  if (m >= a.S) return;
   const int64_t bh = blockIdx.y;
   const int hq = (int)(bh % a.Hq);
   const int64_t b = bh / a.Hq;
@@ -53,277 +104,390 @@ __global__ void __launch_bounds__(256) gather_kernel(GatherArgs a) {
     sk = reinterpret_cast<const T*>(a.kp) + ((b * a.R + r) * a.Hkv + g) * a.D;
     sv = reinterpret_cast<const T*>(a.vp) + ((b * a.R + r) * a.Hkv + g) * a.D;
   }
-  const u32x4 xq = *reinterpret_cast<const u32x4*>(sq + cc * CH);
-  const u32x4 xk = *reinterpret_cast<const u32x4*>(sk + cc * CH);
-  const u32x4 xv = *reinterpret_cast<const u32x4*>(sv + cc * CH);
+  const u32x4 xq = load_raw(sq + cc * CH);
+  const u32x4 xk = load_raw(sk + cc * CH);
+  const u32x4 xv = load_raw(sv + cc * CH);
   *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.qs) + o) = xq;
   *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.ks) + o) = xk;
   *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.vs) + o) = xv;
 }
 
-struct ScatterArgs {
-  const void* os;
-  const int32_t* slot;
-  void* o;
-  int64_t N, S, Ptot;
-  int32_t Hq, D, L;
-  int64_t pw[16];
-  int64_t off[17];
+// ---------------------------------------------------------------- scatter and gather_bwd
+
+struct RunArgs {
+  const void* src;      // [B, Hq, S, D] gathered rows
+  const int32_t* slot;  // [B, Hq, Ptot]
+  void* dst;            // [B, N, H, D]
+  int64_t Ptot;
+  int32_t N, S, D, nruns, run;        // run = positions per run: p (1 when L = 1)
+  int32_t Hq, H, Gs, HC, cpr_shift;   // output head h sums query heads h Gs .. h Gs + Gs - 1
+  int32_t pshift;                     // log2 p when p is a power of two, else -1
+  int32_t pw[16];                     // p^l
+  int32_t off[17];                    // flattened id of entry (l, 0)
+  float inv[16];                      // 1 / p^l
 };
 
-// o[b, j, hq, :]: consecutive threads cover consecutive (hq, chunk) of one base row, so the
-// [B, N, Hq, D] output is written contiguously. The L slot lookups are issued together, then
-// the L row loads, so a thread waits for two memory latencies rather than 2 L.
-template <typename T, int L>
-__global__ void __launch_bounds__(256) scatter_kernel(ScatterArgs a) {
+// Level-l entry (l >= 1) shared by every position of run c: floor(c / p^(l-1)).
+__device__ __forceinline__ int32_t run_entry(const RunArgs& a, uint32_t c, int l) {
+  return (int32_t)(a.pshift >= 0 ? (c >> (a.pshift * (l - 1))) : (c / (uint32_t)a.pw[l - 1]));
+}
+
+// o[b, j, hq, :]. Sum order: levels L-1 .. 1, then level 0; one rounding.
+// PU > 0: runs of at most PU positions, all lookups and loads of a run issued together.
+template <typename T, int L, int PU>
+__global__ void __launch_bounds__(256) scatter_kernel(RunArgs a) {
   constexpr int CH = 16 / sizeof(T);
-  const int CPR = a.D / CH;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t per_row = (int64_t)a.Hq * CPR;
-  const int64_t j = t / per_row;
-  if (j >= a.N) return;
-  const int64_t rem = t % per_row;
-  const int hq = (int)(rem / CPR), cc = (int)(rem % CPR);
-  const int64_t b = blockIdx.y;
+  const uint32_t c = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int hc = blockIdx.y * blockDim.x + threadIdx.x;
+  if (c >= (uint32_t)a.nruns || hc >= a.HC) return;
+  const int hq = hc >> a.cpr_shift, cc = hc & ((1 << a.cpr_shift) - 1);
+  const int64_t b = blockIdx.z;
   const int64_t bh = b * a.Hq + hq;
   const int32_t* sl = a.slot + bh * a.Ptot;
-  const T* src = reinterpret_cast<const T*>(a.os) + bh * a.S * a.D + cc * CH;
-  int32_t m[L];
-#pragma unroll
-  for (int l = L - 1; l >= 0; --l) {
-    const int64_t i = (j + 1) / a.pw[l] - 1;
-    m[l] = i < 0 ? -1 : sl[a.off[l] + i];
-  }
-  float v[L][CH];
-#pragma unroll
-  for (int l = L - 1; l >= 0; --l) {
-    if (m[l] >= 0 && m[l] < a.S) load_chunk<T>(src + (int64_t)m[l] * a.D, v[l]);
-    else {
-#pragma unroll
-      for (int c = 0; c < CH; ++c) v[l][c] = 0.0f;
-    }
-  }
+  const T* src = reinterpret_cast<const T*>(a.src) + bh * a.S * a.D + cc * CH;
   float acc[CH];
 #pragma unroll
-  for (int c = 0; c < CH; ++c) acc[c] = 0.0f;
+  for (int e = 0; e < CH; ++e) acc[e] = 0.0f;
+  if constexpr (L > 1) {
+    int32_t m[L];
 #pragma unroll
-  for (int l = L - 1; l >= 0; --l)
+    for (int l = L - 1; l >= 1; --l) {
+      const int32_t i = run_entry(a, c, l) - 1;
+      m[l] = i >= 0 ? sl[a.off[l] + i] : -1;
+    }
+    u32x4 v[L];
 #pragma unroll
-    for (int c = 0; c < CH; ++c) acc[c] += v[l][c];
-  store_chunk<T>(reinterpret_cast<T*>(a.o) + ((b * a.N + j) * a.Hq + hq) * a.D + cc * CH, acc);
+    for (int l = L - 1; l >= 1; --l)
+      v[l] = (uint32_t)m[l] < (uint32_t)a.S ? load_raw(src + (int64_t)m[l] * a.D) : u32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int l = L - 1; l >= 1; --l) add_chunk<T>(acc, v[l]);
+  }
+  // level 0: position j takes entry (0, j)
+  T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.Hq + hq) * (int64_t)a.D + cc * CH;
+  const int64_t dstride = (int64_t)a.Hq * a.D;
+  const int32_t jbase = (int32_t)(c * (uint32_t)a.run) - 1;
+  if constexpr (PU > 0) {
+    int32_t m0[PU];
+#pragma unroll
+    for (int r = 0; r < PU; ++r) {
+      const int32_t j = jbase + r;
+      m0[r] = (r < a.run && j >= 0 && j < a.N) ? sl[j] : -1;
+    }
+    u32x4 v0[PU];
+#pragma unroll
+    for (int r = 0; r < PU; ++r)
+      v0[r] = (uint32_t)m0[r] < (uint32_t)a.S ? load_raw(src + (int64_t)m0[r] * a.D) : u32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int r = 0; r < PU; ++r) {
+      const int32_t j = jbase + r;
+      if (r < a.run && j >= 0 && j < a.N) {
+        float o[CH];
+#pragma unroll
+        for (int e = 0; e < CH; ++e) o[e] = acc[e];
+        add_chunk<T>(o, v0[r]);
+        store_chunk<T>(dst + (int64_t)j * dstride, o);
+      }
+    }
+  } else {
+    for (int r = 0; r < a.run; ++r) {
+      const int32_t j = jbase + r;
+      if (j < 0 || j >= a.N) continue;
+      const int32_t m0 = sl[j];
+      float o[CH];
+#pragma unroll
+      for (int e = 0; e < CH; ++e) o[e] = acc[e];
+      if ((uint32_t)m0 < (uint32_t)a.S) add_chunk<T>(o, load_raw(src + (int64_t)m0 * a.D));
+      store_chunk<T>(dst + (int64_t)j * dstride, o);
+    }
+  }
 }
+
+// dst[b, j, h, :] = sum over the Gs query heads g of the group and the levels l of
+// src_g[slot_g(l, floor(j/p^l))] / p^l. Sum order: levels L-1 .. 1 of every head in turn, then
+// level 0 of every head in turn; one rounding.
+template <typename T, int L, int PU>
+__global__ void __launch_bounds__(256) gather_bwd_kernel(RunArgs a) {
+  constexpr int CH = 16 / sizeof(T);
+  constexpr int NP = PU > 0 ? PU : 1;
+  const uint32_t c = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int hc = blockIdx.y * blockDim.x + threadIdx.x;
+  if (c >= (uint32_t)a.nruns || hc >= a.HC) return;
+  const int h = hc >> a.cpr_shift, cc = hc & ((1 << a.cpr_shift) - 1);
+  const int64_t b = blockIdx.z;
+  const int32_t jbase = (int32_t)(c * (uint32_t)a.run);
+  int32_t ent[L > 1 ? L : 2];
+#pragma unroll
+  for (int l = 1; l < L; ++l) ent[l] = a.off[l] + run_entry(a, c, l);
+  float acc[CH];
+#pragma unroll
+  for (int e = 0; e < CH; ++e) acc[e] = 0.0f;
+  float fine[NP][CH];
+#pragma unroll
+  for (int r = 0; r < NP; ++r)
+#pragma unroll
+    for (int e = 0; e < CH; ++e) fine[r][e] = 0.0f;
+  T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.H + h) * (int64_t)a.D + cc * CH;
+  const int64_t dstride = (int64_t)a.H * a.D;
+  for (int g = 0; g < a.Gs; ++g) {
+    const int64_t bhq = b * a.Hq + (int64_t)h * a.Gs + g;
+    const int32_t* sl = a.slot + bhq * a.Ptot;
+    const T* src = reinterpret_cast<const T*>(a.src) + bhq * a.S * a.D + cc * CH;
+    int32_t m[L > 1 ? L : 2];
+#pragma unroll
+    for (int l = L - 1; l >= 1; --l) m[l] = sl[ent[l]];
+    int32_t m0[NP];
+    if constexpr (PU > 0) {
+#pragma unroll
+      for (int r = 0; r < PU; ++r) m0[r] = r < a.run ? sl[jbase + r] : -1;
+    }
+    u32x4 v[L > 1 ? L : 2];
+#pragma unroll
+    for (int l = L - 1; l >= 1; --l)
+      v[l] = (uint32_t)m[l] < (uint32_t)a.S ? load_raw(src + (int64_t)m[l] * a.D) : u32x4{0, 0, 0, 0};
+    if constexpr (PU > 0) {
+      u32x4 v0[PU];
+#pragma unroll
+      for (int r = 0; r < PU; ++r)
+        v0[r] = (uint32_t)m0[r] < (uint32_t)a.S ? load_raw(src + (int64_t)m0[r] * a.D) : u32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int l = L - 1; l >= 1; --l) add_chunk_scaled<T>(acc, v[l], a.inv[l]);
+#pragma unroll
+      for (int r = 0; r < PU; ++r) add_chunk<T>(fine[r], v0[r]);
+    } else {
+#pragma unroll
+      for (int l = L - 1; l >= 1; --l) add_chunk_scaled<T>(acc, v[l], a.inv[l]);
+    }
+  }
+  if constexpr (PU > 0) {
+#pragma unroll
+    for (int r = 0; r < PU; ++r) {
+      if (r < a.run) {
+        float o[CH];
+#pragma unroll
+        for (int e = 0; e < CH; ++e) o[e] = acc[e] + fine[r][e];
+        store_chunk<T>(dst + (int64_t)(jbase + r) * dstride, o);
+      }
+    }
+  } else {
+    for (int r = 0; r < a.run; ++r) {
+      float o[CH];
+#pragma unroll
+      for (int e = 0; e < CH; ++e) o[e] = 0.0f;
+      for (int g = 0; g < a.Gs; ++g) {
+        const int64_t bhq = b * a.Hq + (int64_t)h * a.Gs + g;
+        const int32_t m0 = a.slot[bhq * a.Ptot + jbase + r];
+        if ((uint32_t)m0 < (uint32_t)a.S)
+          add_chunk<T>(o, load_raw(reinterpret_cast<const T*>(a.src) + (bhq * a.S + m0) * a.D + cc * CH));
+      }
+#pragma unroll
+      for (int e = 0; e < CH; ++e) o[e] = acc[e] + o[e];
+      store_chunk<T>(dst + (int64_t)(jbase + r) * dstride, o);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- scatter_bwd
 
 struct ScatterBwdArgs {
   const void* dout;  // [B, N, Hq, D]
   const int32_t* slot;
   void* dos;  // [B, Hq, S, D]
-  int64_t N, S, Ptot, WR, U;  // U = N + P: positions of the shifted sequence
-  int32_t Hq, D, HW;
-  int64_t pw[16];
-  int64_t off[17];
-  int64_t nrows[16];
+  int64_t Ptot;
+  int32_t N, S, U, WR, Hq, D, HW, cpr_shift, p;  // U = N + p^(L-1): positions of the shifted sequence
+  int32_t off[17];
+  int32_t nrows[16];  // N / p^l
+  int32_t epb[16];    // WR / p^l: level-l windows per workgroup
 };
+
+constexpr int kScatterBwdRB = 8;  // rows loaded per step
 
 // Shifted window sums. With x[u] = dout[u - 1] (zero for u = 0 and u > N), the range of entry
 // (l, i) is exactly the level-l window a = i + 1 of x: [a p^l, (a+1) p^l - 1]. A workgroup walks
 // a range of u that is a multiple of p^(L-1) with fp32 running sums per level (as in pooling)
-// and writes the sum of every closed window whose entry was gathered. dout is read once.
+// and writes the sum of every closed window whose entry was gathered; level-0 entries are a
+// plain copy. dout is read once. Window closings are tracked with counters, and the slot of a
+// window's entry is fetched when the window opens, so it has arrived when the window closes.
 template <typename T, int L>
-__global__ void __launch_bounds__(1024) scatter_bwd_kernel(ScatterBwdArgs a) {
+__global__ void __launch_bounds__(256) scatter_bwd_kernel(ScatterBwdArgs a) {
   constexpr int CH = 16 / sizeof(T);
-  const int CPR = a.D / CH;
+  constexpr int LA = L > 1 ? L : 2;
+  constexpr int RB = kScatterBwdRB;
   const int tid = threadIdx.x;
-  const int hc = tid / CPR, cc = tid % CPR;
+  const int hc = tid >> a.cpr_shift, cc = tid & ((1 << a.cpr_shift) - 1);
   const int hq = blockIdx.y * a.HW + hc;
-  if (hq >= a.Hq) return;
+  if (hq >= a.Hq) return;  // no barriers below
   const int64_t b = blockIdx.z;
   const int64_t bh = b * a.Hq + hq;
   const int32_t* sl = a.slot + bh * a.Ptot;
   T* dos = reinterpret_cast<T*>(a.dos) + bh * a.S * a.D + cc * CH;
-  const T* src = reinterpret_cast<const T*>(a.dout);
-  const int64_t u0 = (int64_t)blockIdx.x * a.WR;
-  int64_t u1 = u0 + a.WR;
-  if (u1 > a.U) u1 = a.U;
-  float acc[L > 1 ? L : 2][CH];
+  const T* src = reinterpret_cast<const T*>(a.dout) + (b * a.N * a.Hq + hq) * (int64_t)a.D + cc * CH;
+  const int64_t sstride = (int64_t)a.Hq * a.D;
+  const int32_t u0 = (int32_t)blockIdx.x * a.WR;
+  const int32_t nu = a.U - u0 < a.WR ? a.U - u0 : a.WR;
+
+  float acc[LA][CH];
 #pragma unroll
-  for (int l = 0; l < (L > 1 ? L : 2); ++l)
+  for (int l = 0; l < LA; ++l)
 #pragma unroll
-    for (int c = 0; c < CH; ++c) acc[l][c] = 0.0f;
-  constexpr int RB = 4;
-  for (int64_t ub = u0; ub < u1; ub += RB) {
-    float v[RB][CH];
+    for (int e = 0; e < CH; ++e) acc[l][e] = 0.0f;
+  int cnt[LA + 1];
+#pragma unroll
+  for (int l = 0; l <= LA; ++l) cnt[l] = 0;
+  int32_t win[LA];  // index a of the open level-l window; its entry is i = a - 1
+  int32_t ms[LA];   // slot of that entry, or -1
+  auto entry_slot = [&](int l, int32_t i) -> int32_t {
+    return (i >= 0 && i < a.nrows[l]) ? sl[a.off[l] + i] : -1;
+  };
+#pragma unroll
+  for (int l = 1; l < L; ++l) {
+    win[l] = (int32_t)blockIdx.x * a.epb[l];
+    ms[l] = entry_slot(l, win[l] - 1);
+  }
+
+  for (int ub = 0; ub < nu; ub += RB) {
+    u32x4 v[RB];
+    int32_t m0[RB];
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
-      const int64_t u = ub + r;
-      if (u < u1 && u >= 1 && u <= a.N) {
-        load_chunk<T>(src + ((b * a.N + (u - 1)) * a.Hq + hq) * a.D + cc * CH, v[r]);
-      } else {
-#pragma unroll
-        for (int c = 0; c < CH; ++c) v[r][c] = 0.0f;
-      }
+      const int32_t u = u0 + ub + r;
+      const bool valid = ub + r < nu && u >= 1 && u <= a.N;
+      v[r] = valid ? load_raw(src + (int64_t)(u - 1) * sstride) : u32x4{0, 0, 0, 0};
+      m0[r] = valid ? sl[u - 1] : -1;
     }
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
-      const int64_t u = ub + r;
-      if (u >= u1) break;
-      // level 0: entry i = u - 1 takes x[u] = dout[u - 1]
-      if (u >= 1 && u <= a.N) {
-        const int32_t m = sl[u - 1];
-        if (m >= 0 && m < a.S) store_chunk<T>(dos + (int64_t)m * a.D, v[r]);
-      }
-      if (L > 1) {
+      if (ub + r >= nu) break;
+      // level 0: entry i = u - 1 takes x[u] = dout[u - 1] unchanged
+      if ((uint32_t)m0[r] < (uint32_t)a.S) *reinterpret_cast<u32x4*>(dos + (int64_t)m0[r] * a.D) = v[r];
+      if constexpr (L > 1) {
+        add_chunk<T>(acc[1], v[r]);
+        if (++cnt[1] == a.p) {
 #pragma unroll
-        for (int c = 0; c < CH; ++c) acc[1][c] += v[r][c];
+          for (int l = 1; l < L; ++l) {
+            if (l > 1 && cnt[l] != a.p) break;
+            cnt[l] = 0;
+            if ((uint32_t)ms[l] < (uint32_t)a.S) store_chunk<T>(dos + (int64_t)ms[l] * a.D, acc[l]);
+            if (l + 1 < L) {
 #pragma unroll
-        for (int l = 1; l < L; ++l) {
-          if ((u + 1) % a.pw[l] != 0) break;
-          const int64_t i = (u + 1) / a.pw[l] - 2;  // window a = i + 1 closed
-          if (i >= 0 && i < a.nrows[l]) {
-            const int32_t m = sl[a.off[l] + i];
-            if (m >= 0 && m < a.S) store_chunk<T>(dos + (int64_t)m * a.D, acc[l]);
+              for (int e = 0; e < CH; ++e) acc[l + 1 < L ? l + 1 : l][e] += acc[l][e];
+              ++cnt[l + 1 < L ? l + 1 : l];
+            }
+#pragma unroll
+            for (int e = 0; e < CH; ++e) acc[l][e] = 0.0f;
+            ++win[l];
+            ms[l] = entry_slot(l, win[l] - 1);
           }
-          if (l + 1 < L) {
-#pragma unroll
-            for (int c = 0; c < CH; ++c) acc[l + 1 < L ? l + 1 : l][c] += acc[l][c];
-          }
-#pragma unroll
-          for (int c = 0; c < CH; ++c) acc[l][c] = 0.0f;
         }
       }
     }
   }
 }
 
-struct GatherBwdArgs {
-  const void* src;  // [B, Hq, S, D]
-  const int32_t* slot;
-  void* dst;  // [B, N, H, D]
-  int64_t N, S, Ptot;
-  int32_t Hq, H, Gs, D, L;  // output heads H; output head h sums query heads h*Gs .. h*Gs+Gs-1
-  int64_t pw[16];
-  int64_t off[17];
-  float inv[16];
-};
+// ---------------------------------------------------------------- host launchers
 
-// Output head h sums query heads h Gs .. h Gs + Gs - 1 (Gs = G for dK/dV, 1 for dQ) over the
-// levels, in the order (query head ascending, level L-1 first). For each query head the L slot
-// lookups are issued together, then the L row loads; with GS > 0 (compile-time group size) the
-// lookups of all heads go out first.
-template <typename T, int L>
-__device__ __forceinline__ void gather_bwd_head(const GatherBwdArgs& a, const int32_t* m, int64_t bhq, int cc,
-                                                float* acc) {
-  constexpr int CH = 16 / sizeof(T);
-  const T* src = reinterpret_cast<const T*>(a.src) + bhq * a.S * a.D + cc * CH;
-  float v[L][CH];
-#pragma unroll
-  for (int l = L - 1; l >= 0; --l) {
-    if (m[l] >= 0 && m[l] < a.S) load_chunk<T>(src + (int64_t)m[l] * a.D, v[l]);
-    else {
-#pragma unroll
-      for (int c = 0; c < CH; ++c) v[l][c] = 0.0f;
-    }
-  }
-#pragma unroll
-  for (int l = L - 1; l >= 0; --l)
-#pragma unroll
-    for (int c = 0; c < CH; ++c) acc[c] += v[l][c] * a.inv[l];
-}
-
-template <typename T, int L, int GS>
-__global__ void __launch_bounds__(256) gather_bwd_kernel(GatherBwdArgs a) {
-  constexpr int CH = 16 / sizeof(T);
-  const int CPR = a.D / CH;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t per_row = (int64_t)a.H * CPR;
-  const int64_t j = t / per_row;
-  if (j >= a.N) return;
-  const int64_t rem = t % per_row;
-  const int h = (int)(rem / CPR), cc = (int)(rem % CPR);
-  const int64_t b = blockIdx.y;
-  float acc[CH];
-#pragma unroll
-  for (int c = 0; c < CH; ++c) acc[c] = 0.0f;
-  if constexpr (GS > 0) {
-    int32_t m[GS][L];
-#pragma unroll
-    for (int g = 0; g < GS; ++g) {
-      const int32_t* sl = a.slot + (b * a.Hq + (int64_t)h * GS + g) * a.Ptot;
-#pragma unroll
-      for (int l = L - 1; l >= 0; --l) m[g][l] = sl[a.off[l] + j / a.pw[l]];
-    }
-#pragma unroll
-    for (int g = 0; g < GS; ++g) gather_bwd_head<T, L>(a, m[g], b * a.Hq + (int64_t)h * GS + g, cc, acc);
-  } else {
-    for (int g = 0; g < a.Gs; ++g) {
-      const int64_t bhq = b * a.Hq + (int64_t)h * a.Gs + g;
-      const int32_t* sl = a.slot + bhq * a.Ptot;
-      int32_t m[L];
-#pragma unroll
-      for (int l = L - 1; l >= 0; --l) m[l] = sl[a.off[l] + j / a.pw[l]];
-      gather_bwd_head<T, L>(a, m, bhq, cc, acc);
-    }
-  }
-  store_chunk<T>(reinterpret_cast<T*>(a.dst) + ((b * a.N + j) * a.H + h) * a.D + cc * CH, acc);
+static int cpr_shift_of(int D, int esize) {
+  const int cpr = D * esize / 16;
+  int s = 0;
+  while ((1 << s) < cpr) ++s;
+  return s;
 }
 
 template <typename T, int L>
-static void launch_gather_bwd_G(const GatherBwdArgs& a, dim3 grid, hipStream_t st) {
-  switch (a.Gs) {
-    case 1: hipLaunchKernelGGL((gather_bwd_kernel<T, L, 1>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((gather_bwd_kernel<T, L, 2>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((gather_bwd_kernel<T, L, 4>), grid, dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((gather_bwd_kernel<T, L, 8>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((gather_bwd_kernel<T, L, 0>), grid, dim3(256), 0, st, a); break;
-  }
+static void launch_scatter_P(const RunArgs& a, dim3 grid, dim3 block, hipStream_t st) {
+  if (a.run <= 4) hipLaunchKernelGGL((scatter_kernel<T, L, 4>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((scatter_kernel<T, L, 0>), grid, block, 0, st, a);
+}
+
+template <typename T, int L>
+static void launch_gather_bwd_P(const RunArgs& a, dim3 grid, dim3 block, hipStream_t st) {
+  if (a.run <= 4) hipLaunchKernelGGL((gather_bwd_kernel<T, L, 4>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((gather_bwd_kernel<T, L, 0>), grid, block, 0, st, a);
 }
 
 template <typename T>
-static void launch_gather_bwd_L(const GatherBwdArgs& a, dim3 grid, hipStream_t st) {
-  switch (a.L) {
-    case 1: launch_gather_bwd_G<T, 1>(a, grid, st); break;
-    case 2: launch_gather_bwd_G<T, 2>(a, grid, st); break;
-    case 3: launch_gather_bwd_G<T, 3>(a, grid, st); break;
-    case 4: launch_gather_bwd_G<T, 4>(a, grid, st); break;
-    case 5: launch_gather_bwd_G<T, 5>(a, grid, st); break;
-    case 6: launch_gather_bwd_G<T, 6>(a, grid, st); break;
-    case 7: launch_gather_bwd_G<T, 7>(a, grid, st); break;
-    default: launch_gather_bwd_G<T, 8>(a, grid, st); break;
+static void launch_run_kernel(bool scatter, int L, const RunArgs& a, dim3 grid, dim3 block, hipStream_t st) {
+#define LH_RUN_CASE(LL)                                            \
+  case LL:                                                         \
+    if (scatter) launch_scatter_P<T, LL>(a, grid, block, st);      \
+    else launch_gather_bwd_P<T, LL>(a, grid, block, st);           \
+    break;
+  switch (L) {
+    LH_RUN_CASE(1)
+    LH_RUN_CASE(2)
+    LH_RUN_CASE(3)
+    LH_RUN_CASE(4)
+    LH_RUN_CASE(5)
+    LH_RUN_CASE(6)
+    LH_RUN_CASE(7)
+    default: LH_RUN_CASE(8)
   }
+#undef LH_RUN_CASE
 }
 
-template <typename T>
-static void launch_scatter_L(const ScatterArgs& a, dim3 grid, hipStream_t st) {
-  switch (a.L) {
-    case 1: hipLaunchKernelGGL((scatter_kernel<T, 1>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((scatter_kernel<T, 2>), grid, dim3(256), 0, st, a); break;
-    case 3: hipLaunchKernelGGL((scatter_kernel<T, 3>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((scatter_kernel<T, 4>), grid, dim3(256), 0, st, a); break;
-    case 5: hipLaunchKernelGGL((scatter_kernel<T, 5>), grid, dim3(256), 0, st, a); break;
-    case 6: hipLaunchKernelGGL((scatter_kernel<T, 6>), grid, dim3(256), 0, st, a); break;
-    case 7: hipLaunchKernelGGL((scatter_kernel<T, 7>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((scatter_kernel<T, 8>), grid, dim3(256), 0, st, a); break;
+static RunArgs run_args(const LhShape& s, const void* src, const int32_t* slot, void* dst, int H, int Gs,
+                        bool scatter) {
+  RunArgs a = {};
+  a.src = src;
+  a.slot = slot;
+  a.dst = dst;
+  a.Ptot = s.Ptot;
+  a.N = (int32_t)s.N;
+  a.S = (int32_t)s.S;
+  a.D = s.D;
+  a.run = s.L > 1 ? s.p : 1;
+  a.nruns = (int32_t)(s.N / a.run) + (scatter ? 1 : 0);
+  a.Hq = s.Hq;
+  a.H = H;
+  a.Gs = Gs;
+  const int es = s.dtype == LH_BF16 ? 2 : 4;
+  a.cpr_shift = cpr_shift_of(s.D, es);
+  a.HC = H << a.cpr_shift;
+  a.pshift = -1;
+  if (s.L > 1 && (s.p & (s.p - 1)) == 0) {
+    a.pshift = 0;
+    while ((1 << a.pshift) < s.p) ++a.pshift;
   }
+  for (int l = 0; l < 16; ++l) {
+    a.pw[l] = l < s.L ? (int32_t)s.pw[l] : 1;
+    a.inv[l] = l < s.L ? 1.0f / (float)s.pw[l] : 0.0f;
+  }
+  for (int l = 0; l < 17; ++l) a.off[l] = (int32_t)s.off[l];
+  return a;
+}
+
+static void run_grid(const RunArgs& a, int B, dim3* grid, dim3* block) {
+  const int bs = a.HC < 256 ? a.HC : 256;
+  const unsigned nx = (unsigned)((a.nruns + 7) / 8 * 8);  // a multiple of 8 for the XCD mapping
+  *grid = dim3(nx, (unsigned)((a.HC + bs - 1) / bs), (unsigned)B);
+  *block = dim3((unsigned)bs);
 }
 
 template <typename T, int L>
 static hipError_t launch_scatter_bwd_T(const LhShape& s, const void* dout, const int32_t* slot,
                                        void* dos, hipStream_t st) {
-  ScatterBwdArgs a;
+  ScatterBwdArgs a = {};
   a.dout = dout;
   a.slot = slot;
   a.dos = dos;
-  a.N = s.N;
-  a.S = s.S;
   a.Ptot = s.Ptot;
-  a.U = s.N + s.P;
+  a.N = (int32_t)s.N;
+  a.S = (int32_t)s.S;
+  a.U = (int32_t)(s.N + s.P);
   a.Hq = s.Hq;
   a.D = s.D;
-  const int CPR = s.D / (16 / (int)sizeof(T));
+  a.p = s.p;
+  a.cpr_shift = cpr_shift_of(s.D, (int)sizeof(T));
+  const int CPR = 1 << a.cpr_shift;
   a.HW = s.Hq < 256 / CPR ? s.Hq : 256 / CPR;
-  a.WR = s.P >= 64 ? s.P : s.P * ((64 + s.P - 1) / s.P);
-  for (int l = 0; l < 16; ++l) a.pw[l] = s.pw[l], a.nrows[l] = l < s.L ? s.N / s.pw[l] : 0;
-  for (int l = 0; l < 17; ++l) a.off[l] = s.off[l];
-  dim3 grid((unsigned)((a.U + a.WR - 1) / a.WR), (unsigned)((s.Hq + a.HW - 1) / a.HW), (unsigned)s.B);
+  int64_t W = s.P;
+  while (W < 64) W += s.P;
+  a.WR = (int32_t)W;
+  for (int l = 0; l < 16; ++l) {
+    a.nrows[l] = l < s.L ? (int32_t)(s.N / s.pw[l]) : 0;
+    a.epb[l] = l < s.L ? (int32_t)(W / s.pw[l]) : 0;
+  }
+  for (int l = 0; l < 17; ++l) a.off[l] = (int32_t)s.off[l];
+  dim3 grid((unsigned)((a.U + W - 1) / W), (unsigned)((s.Hq + a.HW - 1) / a.HW), (unsigned)s.B);
   hipLaunchKernelGGL((scatter_bwd_kernel<T, L>), grid, dim3((unsigned)(a.HW * CPR)), 0, st, a);
   return hipGetLastError();
 }
@@ -351,10 +515,11 @@ using namespace lh;
 hipError_t lh_launch_gather(const LhShape& s, const void* q, const void* k, const void* v,
                             const void* qpyr, const void* kpyr, const void* vpyr,
                             const int32_t* idx, void* qs, void* ks, void* vs, hipStream_t st) {
-  GatherArgs a{q, k, v, qpyr, kpyr, vpyr, idx, qs, ks, vs, s.N, s.R, s.S, s.Hq, s.Hkv, s.G, s.D};
-  const int CH = s.dtype == LH_BF16 ? 8 : 4;
-  const int64_t n = s.S * (s.D / CH);
-  dim3 grid((unsigned)((n + 255) / 256), (unsigned)(s.B * s.Hq));
+  GatherArgs a{q, k, v, qpyr, kpyr, vpyr, idx, qs, ks, vs, s.N, s.R, s.S, s.Hq, s.Hkv, s.G, s.D, 0, 0};
+  const int es = s.dtype == LH_BF16 ? 2 : 4;
+  a.cpr_shift = cpr_shift_of(s.D, es);
+  a.rows_per_block = 256 >> a.cpr_shift;
+  dim3 grid((unsigned)((s.S + a.rows_per_block - 1) / a.rows_per_block), (unsigned)(s.B * s.Hq));
   if (s.dtype == LH_BF16) hipLaunchKernelGGL(gather_kernel<bf16_t>, grid, dim3(256), 0, st, a);
   else hipLaunchKernelGGL(gather_kernel<float>, grid, dim3(256), 0, st, a);
   return hipGetLastError();
@@ -362,23 +527,11 @@ hipError_t lh_launch_gather(const LhShape& s, const void* q, const void* k, cons
 
 hipError_t lh_launch_scatter(const LhShape& s, const void* os, const int32_t* slot, void* o,
                              hipStream_t st) {
-  ScatterArgs a;
-  a.os = os;
-  a.slot = slot;
-  a.o = o;
-  a.N = s.N;
-  a.S = s.S;
-  a.Ptot = s.Ptot;
-  a.Hq = s.Hq;
-  a.D = s.D;
-  a.L = s.L;
-  for (int l = 0; l < 16; ++l) a.pw[l] = s.pw[l];
-  for (int l = 0; l < 17; ++l) a.off[l] = s.off[l];
-  const int CH = s.dtype == LH_BF16 ? 8 : 4;
-  const int64_t n = s.N * s.Hq * (s.D / CH);
-  dim3 grid((unsigned)((n + 255) / 256), (unsigned)s.B);
-  if (s.dtype == LH_BF16) launch_scatter_L<bf16_t>(a, grid, st);
-  else launch_scatter_L<float>(a, grid, st);
+  const RunArgs a = run_args(s, os, slot, o, s.Hq, 1, true);
+  dim3 grid, block;
+  run_grid(a, (int)s.B, &grid, &block);
+  if (s.dtype == LH_BF16) launch_run_kernel<bf16_t>(true, s.L, a, grid, block, st);
+  else launch_run_kernel<float>(true, s.L, a, grid, block, st);
   return hipGetLastError();
 }
 
@@ -394,28 +547,12 @@ hipError_t lh_launch_gather_bwd(const LhShape& s, const void* dqs, const void* d
   const void* srcs[3] = {dqs, dks, dvs};
   void* dsts[3] = {dq, dk, dv};
   for (int which = 0; which < 3; ++which) {
-    GatherBwdArgs a;
-    a.src = srcs[which];
-    a.slot = slot;
-    a.dst = dsts[which];
-    a.N = s.N;
-    a.S = s.S;
-    a.Ptot = s.Ptot;
-    a.Hq = s.Hq;
-    a.H = which == 0 ? s.Hq : s.Hkv;
-    a.Gs = which == 0 ? 1 : s.G;
-    a.D = s.D;
-    a.L = s.L;
-    for (int l = 0; l < 16; ++l) {
-      a.pw[l] = s.pw[l];
-      a.inv[l] = l < s.L ? 1.0f / (float)s.pw[l] : 0.0f;
-    }
-    for (int l = 0; l < 17; ++l) a.off[l] = s.off[l];
-    const int CH = s.dtype == LH_BF16 ? 8 : 4;
-    const int64_t n = s.N * a.H * (s.D / CH);
-    dim3 grid((unsigned)((n + 255) / 256), (unsigned)s.B);
-    if (s.dtype == LH_BF16) launch_gather_bwd_L<bf16_t>(a, grid, st);
-    else launch_gather_bwd_L<float>(a, grid, st);
+    const RunArgs a = run_args(s, srcs[which], slot, dsts[which], which == 0 ? s.Hq : s.Hkv,
+                               which == 0 ? 1 : s.G, false);
+    dim3 grid, block;
+    run_grid(a, (int)s.B, &grid, &block);
+    if (s.dtype == LH_BF16) launch_run_kernel<bf16_t>(false, s.L, a, grid, block, st);
+    else launch_run_kernel<float>(false, s.L, a, grid, block, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -169,3 +169,19 @@ def test_output_linear_in_v(rng):
     f = oracle.layer_forward(q, k, v, p=p, L=L, kk=kk, dtype=oracle.F64)
     g = oracle.layer_backward(f, dout)
     assert np.isclose((dout * f["o"]).sum(), (g["dv"] * v).sum(), rtol=1e-10, atol=0)
+
+
+def test_row_list_sdpa_matches_full_rows(rng):
+    """The sampled-row SDPA entry points give the same rows as the full computation."""
+    S, D = 300, 16
+    qs, ks, vs, dos = (rng.standard_normal((S, D)) for _ in range(4))
+    sc = 0.25
+    os_full, lse_full = oracle.sdpa_fwd(qs, ks, vs, sc)
+    dq_full, _, _ = oracle.sdpa_bwd(qs, ks, vs, os_full, lse_full, dos, sc)
+    rows = np.array([0, 1, 57, 150, 298, 299])
+    os_r, lse_r = oracle.sdpa_fwd(qs, ks, vs, sc, row_list=rows)
+    assert np.array_equal(os_r[rows], os_full[rows]) and np.array_equal(lse_r[rows], lse_full[rows])
+    other = np.setdiff1d(np.arange(S), rows)
+    assert not os_r[other].any() and not lse_r[other].any()
+    dq_r = oracle.sdpa_bwd_dq_rows(qs, ks, vs, os_r, lse_r, dos, sc, rows)
+    assert np.array_equal(dq_r[rows], dq_full[rows]) and not dq_r[other].any()
