@@ -14,6 +14,7 @@ bounded sample of the same workload and extrapolates it by work counts.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -58,6 +59,35 @@ def stage_work(pr, S, Ptot, es):
     }
 
 
+COPY_PROBE_BYTES = 1 << 30  # the calibration kernel reads and writes this many bytes
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sdpa_bwd_c4.txt")
+SDPA_SOURCES = ("k_sdpa_mfma.hip", "k_sdpa.hip")
+
+
+def sdpa_sources_sha256():
+    h = hashlib.sha256()
+    for f in SDPA_SOURCES:
+        with open(os.path.join(ROOT, "paper_2605_06554_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per call of `kernel` from the committed counter summary, or None when it is
+    missing, covers another stage or workload, or was taken on different kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            kv = dict(ln.split(":", 1) for ln in fh.read().splitlines() if ":" in ln and not ln.startswith(" "))
+    except OSError:
+        return None
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    if kv.get("stage") != kernel or kv.get("workload") != workload:
+        return None
+    if kv.get("sources_sha256") != sdpa_sources_sha256():
+        return None
+    return int(kv["traffic_bytes_per_call"])
+
+
 def run_gpu(args, cfg):
     import paper_2605_06554_amd as lh
 
@@ -89,6 +119,27 @@ def run_gpu(args, cfg):
     def step():
         lh.lh_attention_fwd(pr, q, k, v, o, idx, slot, qs, ks, vs, os_, lse, wsf, stream=stream)
         lh.lh_attention_bwd(pr, idx, slot, qs, ks, vs, os_, lse, dout, dq, dk, dv, wsb, stream=stream)
+
+    if args.traffic_probe:
+        # one forward (state for the backward), the adjoint of the scatter, then exactly one call
+        # of the SDPA backward, then a plain streaming kernel of known size for the counter scale
+        lh.lh_attention_fwd(pr, q, k, v, o, idx, slot, qs, ks, vs, os_, lse, wsf, stream=stream)
+        dos1, dqs1, dks1, dvs1 = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(4))
+        wsd1 = lh.workspace(pr, lh.LH_OP_SDPA_BWD, dev)
+        lh.lh_scatter_bwd(pr, dout, slot, dos1, stream=stream)
+        torch.cuda.synchronize()
+        print("[probe] sdpa_bwd call", file=sys.stderr, flush=True)
+        lh.lh_sdpa_bwd(pr, qs, ks, vs, os_, lse, dos1, dqs1, dks1, dvs1, wsd1, stream=stream)
+        torch.cuda.synchronize()
+        n = COPY_PROBE_BYTES // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        print(f"[probe] copy kernel: reads {COPY_PROBE_BYTES} B, writes {COPY_PROBE_BYTES} B", file=sys.stderr, flush=True)
+        torch.add(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        print("[probe] done", file=sys.stderr, flush=True)
+        return None
 
     for _ in range(args.warmup):
         step()
@@ -154,12 +205,12 @@ def run_gpu(args, cfg):
     if bound == "mfma":
         ach = amount / (ms * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(ach, 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                    frac=round(ach / PEAK_BF16_TFLOPS, 4), traffic=None, kernel=dom,
+                    frac=round(ach / PEAK_BF16_TFLOPS, 4), traffic=measured_traffic(dom, cfg.name), kernel=dom,
                     per_launch=amount, per_launch_unit="FLOP")
     else:
         ach = amount / (ms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s",
-                    frac=round(ach / PEAK_HBM_GBS, 4), traffic=None, kernel=dom,
+                    frac=round(ach / PEAK_HBM_GBS, 4), traffic=measured_traffic(dom, cfg.name), kernel=dom,
                     per_launch=amount, per_launch_unit="B")
     mem_ms = sum(per_stage[n]["ms"] for n in per_stage if work[n][0] == "hbm")
     mem_bytes = sum(work[n][1] for n in per_stage if work[n][0] == "hbm")
@@ -241,6 +292,8 @@ def main():
     ap.add_argument("--config", default="c4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=512)
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="run one SDPA backward call and one copy kernel (for rocprofv3 --pmc), then exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -249,6 +302,9 @@ def main():
               file=sys.stderr)
         raise SystemExit(2)
     cfg = workloads.CONFIGS[args.config]
+    if args.traffic_probe:
+        run_gpu(args, cfg)
+        return
     ms_step, roof, summary, shape = run_gpu(args, cfg)
     B, N = shape[0], shape[1]
     value = B * N / (ms_step * 1e-3)
