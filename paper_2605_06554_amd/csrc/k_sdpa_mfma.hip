@@ -460,8 +460,12 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
       (BUF ? ds1 : ds0)[tid] = q < S ? Dh[q] : 0.0f;
     }
   };
+  // Query tiles are visited from the last one down to the diagonal: every key block of a head
+  // then starts on the same tile and streams the same tiles in step with the others, so the
+  // blocks running together on an XCD share each Q / dO tile through its L2.
+  const int qlast = qstart + (nqt - 1) * CQ;
   load_tile<D, CK, KWV>(Kw, Kh, k0, S, w, lane);
-  stage(IC<0>{}, qstart);
+  stage(IC<0>{}, qlast);
 
   const int krow = mykey < S ? mykey : S - 1;
   bf16x8 vreg[D / 16];
@@ -477,9 +481,9 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
     const bf16_t* dOt = BUF ? dOs1 : dOs0;
     const float* lt = BUF ? ls1 : ls0;
     const float* dt = BUF ? ds1 : ds0;
-    const int qt0 = qstart + it * CQ;
+    const int qt0 = qlast - it * CQ;
     sync_tiles<0>();  // this tile (and its lse / Delta) landed; the other slot is free
-    if (it + 1 < nqt) stage(IC<BUF ^ 1>{}, qt0 + CQ);
+    if (it + 1 < nqt) stage(IC<BUF ^ 1>{}, qt0 - CQ);
     if (qt0 + CQ - 1 < kw || kw >= S) return;  // every query of the tile precedes this wave's keys
     const bool diag = qt0 < kw + 31;
 #pragma unroll
