@@ -24,6 +24,8 @@ _LIB = os.path.join(_HERE, "liblh_oracle.so")
 
 F32, BF16, F64 = 0, 1, 2  # F64: unrounded pooled storage (finite-difference pins)
 REPLACE_PARENTS = 1
+STRATIFIED = 2
+STRAT_CHUNK = 2048  # chunk of the stratified selection (App. D.2)
 
 
 def build(force: bool = True) -> str:

@@ -29,6 +29,10 @@
 #define LHO_BF16 1
 #define LHO_F64 2 /* unrounded storage: used by finite-difference and adjoint pins */
 #define LHO_REPLACE_PARENTS 1u
+#define LHO_STRATIFIED 2u
+/* Chunk of the stratified selection: the paper's chunked top-k cuts the score stream into
+   chunks of 2048 scores (App. D.2). */
+#define LHO_STRAT_CHUNK 2048
 
 typedef struct {
   int64_t N;      /* base sequence length                 */
@@ -176,6 +180,10 @@ static int ord_cmp(const void* a, const void* b) {
      picked through either stream enters as its own triple); the first min(k, |E_l|) are the
      parents; E_{l-1} = the p children {p i + r} of every parent.
      Emitted = union of all E_l (with LHO_REPLACE_PARENTS, parents of levels >= 1 are left out).
+     With LHO_STRATIFIED, a level that ranks (k < |E_l|) takes its parents chunk by chunk: E_l in
+     index order is cut into chunks of LHO_STRAT_CHUNK, and chunk [s, e) contributes its best
+     floor(k e / |E_l|) - floor(k s / |E_l|) candidates (App. D.2 keeps a fixed-size top-m per
+     chunk; sizing the shares from k keeps S and every shape of the exact mode).
    Causal order: entry (l, i) has window end e = (i+1) p^l - 1; entries are sorted by
    key = e L + (L - 1 - l), i.e. by e ascending with the coarser level first on equal e.
    Writes idx[0..S) (flattened ids in causal order), slot[Ptot] (position in idx or -1) and
@@ -206,11 +214,25 @@ int64_t lho_select(const lho_head* h, const float* s_qk, const float* s_kq, int3
         ranked[t].c = a > b ? a : b;
         ranked[t].i = cand[t];
       }
-      qsort(ranked, (size_t)n_cand, sizeof(cand_t), cand_cmp);
       n_par = n_cand < h->k ? n_cand : h->k;
       par = (int64_t*)malloc((size_t)(n_par > 0 ? n_par : 1) * sizeof(int64_t));
       if (!par) return -1;
-      for (int64_t t = 0; t < n_par; ++t) par[t] = ranked[t].i;
+      if ((h->flags & LHO_STRATIFIED) && n_par < n_cand) {
+        /* stratified (App. D.2): the candidates, in index order, are cut into chunks of
+           LHO_STRAT_CHUNK; chunk [s, e) keeps the best floor(k e / n) - floor(k s / n) of its
+           own candidates, so every chunk contributes its share and the level still keeps k */
+        int64_t np = 0;
+        for (int64_t s0 = 0; s0 < n_cand; s0 += LHO_STRAT_CHUNK) {
+          const int64_t e0 = s0 + LHO_STRAT_CHUNK < n_cand ? s0 + LHO_STRAT_CHUNK : n_cand;
+          const int64_t quota = (h->k * e0) / n_cand - (h->k * s0) / n_cand;
+          qsort(ranked + s0, (size_t)(e0 - s0), sizeof(cand_t), cand_cmp);
+          for (int64_t t = 0; t < quota; ++t) par[np++] = ranked[s0 + t].i;
+        }
+        if (np != n_par) return -1;
+      } else {
+        qsort(ranked, (size_t)n_cand, sizeof(cand_t), cand_cmp);
+        for (int64_t t = 0; t < n_par; ++t) par[t] = ranked[t].i;
+      }
       qsort(par, (size_t)n_par, sizeof(int64_t), cmp_i64);
       free(ranked);
     }

@@ -124,3 +124,35 @@ def all_pyramid_attention(q, k, v, p, L, scale):
             if j < N:
                 O[j] += om
     return O
+
+
+def select_stratified(sqk_levels, skq_levels, p, L, k, chunk):
+    """Stratified per-level descent: a level that ranks (k < #candidates) cuts its candidates,
+    in index order, into chunks of `chunk`; chunk [s, e) keeps the first
+    floor(k e / n) - floor(k s / n) distinct entries of the concatenated QK and KQ streams of
+    its own candidates, walked in (score desc, index asc) order. Returns the emitted sets."""
+    cand = list(range(len(sqk_levels[L - 1])))
+    emitted = [None] * L
+    for l in range(L - 1, -1, -1):
+        emitted[l] = sorted(cand)
+        if l == 0:
+            break
+        n = len(cand)
+        parents = []
+        if k >= n:
+            parents = list(cand)
+        else:
+            for s0 in range(0, n, chunk):
+                part = cand[s0:s0 + chunk]
+                quota = (k * (s0 + len(part))) // n - (k * s0) // n
+                stream = [(float(sqk_levels[l][i]), i) for i in part] + [(float(skq_levels[l][i]), i) for i in part]
+                stream.sort(key=lambda t: (-t[0], t[1]))
+                seen = []
+                for _, i in stream:
+                    if len(seen) >= quota:
+                        break
+                    if i not in seen:
+                        seen.append(i)
+                parents += seen
+        cand = sorted(p * i + r for i in parents for r in range(p))
+    return emitted

@@ -166,3 +166,45 @@ def test_spikes_are_selected():
         k = inp["k"][0, :, hq, :].double().numpy()
         idx, slot = oracle.select(h, oracle.scores(h, q), oracle.scores(h, k))
         assert (slot[pos] >= 0).all()
+
+
+# ---------------------------------------------------------------- stratified selection (App. D.2)
+
+@pytest.mark.parametrize("N,p,L,k,ties", [
+    (8192, 2, 3, 1500, False), (8192, 2, 3, 1500, True), (65536, 4, 2, 3000, False), (6561, 3, 3, 900, True),
+])
+def test_stratified_matches_bruteforce(N, p, L, k, ties, rng):
+    s_qk, s_kq, lq, lk = _random_levels(rng, N, p, L, ties)
+    h = oracle.Head(N, 4, p, L, k, oracle.F32, oracle.STRATIFIED)
+    idx, slot = oracle.select(h, s_qk, s_kq)
+    emitted = brute.select_stratified(lq, lk, p, L, k, oracle.STRAT_CHUNK)
+    order = brute.causal_sorted(emitted, N, p, L)
+    assert idx.tolist() == [h.level_offset(l) + i for (l, i) in order]
+    # the shapes of the exact mode are kept
+    h_exact = oracle.Head(N, 4, p, L, k, oracle.F32)
+    assert len(idx) == len(oracle.select(h_exact, s_qk, s_kq)[0])
+
+
+def test_stratified_single_chunk_is_exact(rng):
+    # every level ranks at most 2048 candidates: one chunk, the exact top-k
+    N, p, L, k = 4096, 4, 4, 100
+    s_qk, s_kq, _, _ = _random_levels(rng, N, p, L, True)
+    a = oracle.select(oracle.Head(N, 4, p, L, k, oracle.F32, oracle.STRATIFIED), s_qk, s_kq)[0]
+    b = oracle.select(oracle.Head(N, 4, p, L, k, oracle.F32), s_qk, s_kq)[0]
+    assert a.tolist() == b.tolist()
+
+
+def test_stratified_every_chunk_contributes():
+    # all high scores in the first chunk: the exact top-k takes all of them, the stratified
+    # selection takes each chunk's share (8 chunks of 2048 candidates, 375 parents each)
+    N, p, L, k = 65536, 4, 2, 3000
+    h = oracle.Head(N, 4, p, L, k, oracle.F32, oracle.STRATIFIED)
+    s = np.zeros(h.ptot, np.float32)
+    s[h.level_offset(1): h.level_offset(1) + 2048] = 1.0 + np.arange(2048, dtype=np.float32)
+    idx, _ = oracle.select(h, s, s)
+    parents = sorted({int(t) // p for t in idx if t < h.level_offset(1)})
+    per_chunk = np.bincount(np.array(parents) // oracle.STRAT_CHUNK, minlength=8)
+    assert per_chunk.tolist() == [375] * 8
+    exact = oracle.select(oracle.Head(N, 4, p, L, k, oracle.F32), s, s)[0]
+    par_exact = sorted({int(t) // p for t in exact if t < h.level_offset(1)})
+    assert np.bincount(np.array(par_exact) // oracle.STRAT_CHUNK, minlength=8)[0] == 2048
