@@ -85,7 +85,13 @@ enum {
   /* Test-only selection variant: parents of levels >= 1 are NOT emitted (only their
      descendants are). With a budget that covers every entry it leaves exactly level 0,
      i.e. plain causal SDPA, which pins the gather/SDPA/scatter chain. */
-  LH_FLAG_REPLACE_PARENTS = 1u << 0
+  LH_FLAG_REPLACE_PARENTS = 1u << 0,
+  /* Stratified selection (App. D.2, the chunked top-k the paper implements): a level that
+     ranks its candidates (k < #cand) cuts them, in index order, into chunks of 2048; chunk
+     [s, e) keeps its best floor(k e / #cand) - floor(k s / #cand) candidates by the same key
+     and tie-break. Every chunk of the sequence contributes its share, the level still keeps
+     k parents, and S and every shape are those of the exact mode. */
+  LH_FLAG_STRATIFIED = 1u << 1
 };
 
 /* workspace owners for lh_workspace_bytes */

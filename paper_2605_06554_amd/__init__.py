@@ -14,7 +14,7 @@ import os
 import torch
 
 __all__ = [
-    "LH_OK", "LH_F32", "LH_BF16", "LH_FLAG_REPLACE_PARENTS", "LH_OP_SELECT", "LH_OP_SDPA_BWD",
+    "LH_OK", "LH_F32", "LH_BF16", "LH_FLAG_REPLACE_PARENTS", "LH_FLAG_STRATIFIED", "LH_OP_SELECT", "LH_OP_SDPA_BWD",
     "LH_OP_ATTENTION_FWD", "LH_OP_ATTENTION_BWD", "LighthouseError", "lh_problem", "problem",
     "lh_check", "lh_level_rows", "lh_level_offset", "lh_pyramid_rows", "lh_subseq_len",
     "lh_workspace_bytes", "lh_status_str", "lh_last_error", "lh_pyramid_pool", "lh_score",
@@ -27,6 +27,7 @@ __all__ = [
 LH_OK = 0
 LH_F32, LH_BF16 = 0, 1
 LH_FLAG_REPLACE_PARENTS = 1
+LH_FLAG_STRATIFIED = 2
 LH_OP_SELECT, LH_OP_SDPA_BWD, LH_OP_ATTENTION_FWD, LH_OP_ATTENTION_BWD = 0, 1, 2, 3
 
 _HERE = os.path.dirname(os.path.abspath(__file__))

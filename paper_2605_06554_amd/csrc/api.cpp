@@ -34,7 +34,8 @@ lh_status make_shape(const lh_problem* pr, LhShape* s) {
   if (pr->L > 1 && pr->p < 2) return fail(LH_E_PARAM, "pooling factor p must be >= 2 when L > 1 (p=%d)", pr->p);
   if (pr->k < 0) return fail(LH_E_PARAM, "budget k must be >= 0 (k=%d)", pr->k);
   if (pr->dtype != LH_F32 && pr->dtype != LH_BF16) return fail(LH_E_DTYPE, "dtype must be LH_F32 or LH_BF16 (%d)", pr->dtype);
-  if (pr->flags & ~(uint32_t)LH_FLAG_REPLACE_PARENTS) return fail(LH_E_PARAM, "unknown flag bits 0x%x", pr->flags);
+  if (pr->flags & ~(uint32_t)(LH_FLAG_REPLACE_PARENTS | LH_FLAG_STRATIFIED))
+    return fail(LH_E_PARAM, "unknown flag bits 0x%x", pr->flags);
   if (!(pr->scale == pr->scale) || isinf(pr->scale)) return fail(LH_E_PARAM, "scale must be finite");
   memset(s, 0, sizeof(*s));
   s->B = pr->B;

@@ -457,7 +457,7 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
     if (tid < CQ) {
       const int q = qt0 + tid;
       (BUF ? ls1 : ls0)[tid] = q < S ? Lh[q] * kLog2e : INFINITY;  // rows past S: P = 0
-      (BUF ? ds1 : ds0)[tid] = q < S ? Dh[q] : 0.0f;
+      (BUF ? ds1 : ds0)[tid] = q < S ? -Dh[q] : 0.0f;  // negated: it seeds the dP accumulator
     }
   };
   // Query tiles are visited from the last one down to the diagonal: every key block of a head
@@ -488,7 +488,13 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
     const bool diag = qt0 < kw + 31;
 #pragma unroll
     for (int qb = 0; qb < CQ / 32; ++qb) {
-      f32x16 sacc = f32x16{}, pacc = f32x16{};
+      // the dP accumulator starts at -Delta (stored negated), so it ends as dP - Delta
+      f32x16 sacc = f32x16{}, pacc;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {  // rows qb * 32 + 8 g + 4 h + 0..3 of the C layout
+        const float4 d4 = *reinterpret_cast<const float4*>(dt + qb * 32 + 8 * g + 4 * h);
+        pacc[4 * g + 0] = d4.x, pacc[4 * g + 1] = d4.y, pacc[4 * g + 2] = d4.z, pacc[4 * g + 3] = d4.w;
+      }
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) {
         sacc = mfma32(row8(Qt, qb * 32 * RB + lo.row[kk]), row8(Kw, w * 32 * RB + lo.row[kk]), sacc);
@@ -502,16 +508,14 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
         for (int g = 0; g < 2; ++g) {
           const int qg = qb * 32 + 16 * u + 8 * g + 4 * h;  // tile rows qg .. qg + 3
           const float4 l4 = *reinterpret_cast<const float4*>(lt + qg);
-          const float4 d4 = *reinterpret_cast<const float4*>(dt + qg);
           const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-          const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int i = 8 * u + 4 * g + j;
             float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[i], sl2, -lv[j]));
             if (diag && mykey > qt0 + qg + j) pv = 0.0f;
             pf[4 * g + j] = pv;
-            df[4 * g + j] = pv * (pacc[i] - dv[j]);
+            df[4 * g + j] = pv * pacc[i];
           }
         }
         const bf16x8 pb = cvt8(pf), db = cvt8(df);

@@ -8,6 +8,8 @@
 // histograms with integer atomics). A stable compaction in candidate order then takes every
 // key above the threshold and the first (lower-index) ties, and writes the p children of each
 // parent -- which are the next level's candidates, already sorted -- into the workspace.
+// With LH_FLAG_STRATIFIED (App. D.2) the same select and compaction run on every chunk of 2048
+// consecutive candidates, each keeping its proportional share of the k parents.
 // No floating-point atomics: the result is bitwise deterministic.
 //
 // order_kernel: one thread per candidate. Emitted entries are sorted by
@@ -19,6 +21,8 @@
 namespace lh {
 
 constexpr int kSelThreads = 1024;
+// Stratified mode (App. D.2): candidates of a ranking level are cut into chunks of this many.
+constexpr int64_t kStratChunk = 2048;
 constexpr int kSelWaves = kSelThreads / 64;
 
 struct SelArgs {
@@ -31,6 +35,7 @@ struct SelArgs {
   int64_t cand[16];
   int64_t npar[16];
   int64_t coff[17];
+  int32_t stratified;  // LH_FLAG_STRATIFIED: per-chunk shares instead of one top-k per level
 };
 
 // Exclusive prefix sum over the 1024 threads of the block; returns the exclusive value and
@@ -98,57 +103,69 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
       const float x = sql[i], y = skl[i];
       keys[u] = __float_as_uint(x > y ? x : y);
     }
-    if (tid == 0) {
-      sel_state[0] = 0u;
-      sel_state[1] = (uint32_t)kk;
-    }
     __syncthreads();
-    // MSB-first radix select of the kk-th largest key
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int t = tid; t < 256; t += kSelThreads) hist[t] = 0;
-      __syncthreads();
-      const uint32_t prefix = sel_state[0];
-      const uint32_t himask = shift == 24 ? 0u : (0xffffffffu << (shift + 8));
-      for (int64_t u = tid; u < n; u += kSelThreads) {
-        const uint32_t key = keys[u];
-        if ((key & himask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
-      }
-      __syncthreads();
+    // One chunk covers the whole level in the exact mode. In the stratified mode chunk [s0, e0)
+    // keeps its best floor(kk e0 / n) - floor(kk s0 / n) candidates, written after the
+    // floor(kk s0 / n) parents of the chunks before it (candidate order is kept).
+    const int64_t chunk = a.stratified ? kStratChunk : n;
+    for (int64_t s0 = 0; s0 < n; s0 += chunk) {
+      const int64_t e0 = s0 + chunk < n ? s0 + chunk : n;
+      const int64_t first = a.stratified ? (kk * s0) / n : 0;
+      const int64_t quota = a.stratified ? (kk * e0) / n - first : kk;
+      if (quota == 0) continue;
       if (tid == 0) {
-        uint32_t rem = sel_state[1];
-        int bin = 255;
-        for (; bin > 0; --bin) {
-          const uint32_t c = (uint32_t)hist[bin];
-          if (c >= rem) break;
-          rem -= c;
-        }
-        sel_state[0] = prefix | ((uint32_t)bin << shift);
-        sel_state[1] = rem;
+        sel_state[0] = 0u;
+        sel_state[1] = (uint32_t)quota;
       }
       __syncthreads();
-    }
-    const uint32_t T = sel_state[0];
-    const int need = (int)sel_state[1];  // ties at T to take, lowest candidate positions first
-    // stable compaction in candidate order (rounds of 1024 consecutive candidates)
-    int gt_before = 0, eq_before = 0;
-    for (int64_t base = 0; base < n; base += kSelThreads) {
-      const int64_t u = base + tid;
-      uint32_t key = 0;
-      if (u < n) key = keys[u];
-      const int gt = (u < n && key > T) ? 1 : 0;
-      const int eq = (u < n && key == T) ? 1 : 0;
-      int tot;
-      const int packed = block_exclusive_scan((gt << 16) | eq, scan_sh, &tot);
-      const int gt_rank = gt_before + (packed >> 16);
-      const int eq_rank = eq_before + (packed & 0xffff);
-      const bool take = gt || (eq && eq_rank < need);
-      if (take) {
-        const int pos = gt_rank + (eq_rank < need ? eq_rank : need);
-        const int32_t i = Cl[u];
-        for (int r = 0; r < p; ++r) Cn[(int64_t)pos * p + r] = i * p + r;
+      // MSB-first radix select of the quota-th largest key of the chunk
+      for (int shift = 24; shift >= 0; shift -= 8) {
+        for (int t = tid; t < 256; t += kSelThreads) hist[t] = 0;
+        __syncthreads();
+        const uint32_t prefix = sel_state[0];
+        const uint32_t himask = shift == 24 ? 0u : (0xffffffffu << (shift + 8));
+        for (int64_t u = s0 + tid; u < e0; u += kSelThreads) {
+          const uint32_t key = keys[u];
+          if ((key & himask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+        }
+        __syncthreads();
+        if (tid == 0) {
+          uint32_t rem = sel_state[1];
+          int bin = 255;
+          for (; bin > 0; --bin) {
+            const uint32_t c = (uint32_t)hist[bin];
+            if (c >= rem) break;
+            rem -= c;
+          }
+          sel_state[0] = prefix | ((uint32_t)bin << shift);
+          sel_state[1] = rem;
+        }
+        __syncthreads();
       }
-      gt_before += tot >> 16;
-      eq_before += tot & 0xffff;
+      const uint32_t T = sel_state[0];
+      const int need = (int)sel_state[1];  // ties at T to take, lowest candidate positions first
+      // stable compaction in candidate order (rounds of 1024 consecutive candidates)
+      int gt_before = 0, eq_before = 0;
+      for (int64_t base = s0; base < e0; base += kSelThreads) {
+        const int64_t u = base + tid;
+        uint32_t key = 0;
+        if (u < e0) key = keys[u];
+        const int gt = (u < e0 && key > T) ? 1 : 0;
+        const int eq = (u < e0 && key == T) ? 1 : 0;
+        int tot;
+        const int packed = block_exclusive_scan((gt << 16) | eq, scan_sh, &tot);
+        const int gt_rank = gt_before + (packed >> 16);
+        const int eq_rank = eq_before + (packed & 0xffff);
+        const bool take = gt || (eq && eq_rank < need);
+        if (take) {
+          const int64_t pos = first + gt_rank + (eq_rank < need ? eq_rank : need);
+          const int32_t i = Cl[u];
+          for (int r = 0; r < p; ++r) Cn[pos * p + r] = i * p + r;
+        }
+        gt_before += tot >> 16;
+        eq_before += tot & 0xffff;
+      }
+      __syncthreads();  // sel_state and hist are reused by the next chunk
     }
     __threadfence_block();
     __syncthreads();
@@ -258,6 +275,7 @@ hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_
   a.p = s.p;
   for (int l = 0; l < 17; ++l) a.off[l] = s.off[l], a.coff[l] = s.coff[l];
   for (int l = 0; l < 16; ++l) a.cand[l] = s.cand[l], a.npar[l] = s.npar[l];
+  a.stratified = (s.flags & LH_FLAG_STRATIFIED) ? 1 : 0;
   const size_t shm = (size_t)(s.maxsel > 0 ? s.maxsel : 1) * sizeof(uint32_t);
   hipLaunchKernelGGL(select_kernel, dim3((unsigned)BH), dim3(kSelThreads), shm, st, a);
   hipError_t e = hipGetLastError();

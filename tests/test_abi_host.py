@@ -81,7 +81,7 @@ def test_shapes_match_oracle(name, rng):
         assert lh.lh_subseq_len(pr) == len(idx)
 
 
-@pytest.mark.parametrize("flags", [0, lh.LH_FLAG_REPLACE_PARENTS])
+@pytest.mark.parametrize("flags", [0, lh.LH_FLAG_REPLACE_PARENTS, lh.LH_FLAG_STRATIFIED])
 @pytest.mark.parametrize("N,p,L,k", [(64, 2, 4, 3), (256, 4, 4, 300), (81, 3, 3, 4), (777, 4, 1, 0)])
 def test_subseq_len_matches_oracle_selection(N, p, L, k, flags, rng):
     pr = lh.problem(1, N, 1, 1, 64, p, L, k, lh.LH_F32, 0.0, flags)

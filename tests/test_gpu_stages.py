@@ -105,7 +105,10 @@ def test_select_fig2_toy():
 
 @pytest.mark.parametrize("ties", [False, True])
 @pytest.mark.parametrize("N,p,L,k,flags", [(4096, 4, 4, 100, 0), (4096, 4, 4, 100, 1), (2048, 2, 6, 37, 0),
-                                           (2187, 3, 3, 50, 1), (16384, 4, 5, 4096, 0), (65536, 4, 3, 8192, 0)])
+                                           (2187, 3, 3, 50, 1), (16384, 4, 5, 4096, 0), (65536, 4, 3, 8192, 0),
+                                           # stratified: several chunks of 2048 candidates per level
+                                           (65536, 4, 3, 8192, 2), (65536, 4, 2, 3000, 2), (8192, 2, 3, 1500, 3),
+                                           (6561, 3, 3, 900, 2)])
 def test_select_random_scores(N, p, L, k, flags, ties, rng):
     Hq, Hkv = 4, 2
     print(f"[stage select] N={N} p={p} L={L} k={k} flags={flags} ties={ties}", flush=True)

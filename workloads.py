@@ -71,6 +71,9 @@ TEST_CONFIGS = {
     "t_l1": Config("t_l1", 1, 777, 2, 2, 128, 4, 1, 0, "bf16", 2004),
     # k = 0: only the coarsest level
     "t_k0": Config("t_k0", 1, 1024, 2, 2, 128, 4, 3, 0, "bf16", 2005),
+    # stratified selection (flag bit 1): levels 2 and 1 rank 4096 and 3000 candidates in chunks
+    # of 2048, S = 4096 + 3000 + 3000
+    "t_strat": Config("t_strat", 1, 16384, 2, 1, 64, 2, 3, 1500, "bf16", 2006, "spikes", 0.01, flags=2),
 }
 
 
