@@ -19,11 +19,14 @@
 // LDS tiles: rows of D bf16 (2D bytes, no padding) with an XOR swizzle of 16-byte chunks
 // (chunk c of row r sits at position c ^ swz(r)), filled straight from global memory with
 // global_load_lds_dwordx4 (no staging registers), double-buffered so the next tile streams in
-// while the current one is used. The swizzle makes both read patterns bank-conflict free:
-// 16 consecutive rows reading one logical chunk (b128 operand reads) land on 16 different
-// chunk positions, and the 4 consecutive rows of a transposed read, each reading an aligned
-// group of 4 chunks, land in 4 different groups. Every lane's LDS offsets are computed once;
-// tile bases are compile-time constants (the tile loop is unrolled over the ring of slots).
+// while the current one is used. The forward and dQ kernels use a swizzle under which both read
+// patterns are bank-conflict free (measured with SQ_LDS_BANK_CONFLICT): 16 consecutive rows
+// reading one logical chunk (b128 operand reads) land on 16 different chunk positions, and the
+// 4 consecutive rows of a transposed read, each reading an aligned group of 4 chunks, land in 4
+// different groups. The dK/dV kernel, short of registers, uses a swizzle of r % 8 that keeps
+// the transposed reads conflict free and costs a 2-way conflict on its row reads. Every lane's
+// LDS offsets are computed once; tile bases are compile-time constants (the tile loop is
+// unrolled over the ring of slots).
 //
 // Pipeline: each kernel keeps an NS-slot ring of tiles in LDS. Before using tile t, a wave
 // waits until at most (NS - 2) tiles' worth of its own LDS-DMA loads are outstanding (vmcnt
@@ -81,19 +84,32 @@ using IC = std::integral_constant<int, N>;
 // D = 128 (16 chunks per row): swap the two 2-bit halves of r % 16.
 // D = 64 (8 chunks per row, two rows per 256-byte bank line): a bijection of (r / 2) % 8 whose
 // top bit follows bit 1 of r.
-#ifndef LH_SWZ
-#define LH_SWZ 3
+// Two swizzles of the 16-byte chunks of a row (SW below):
+//   SW = 2: a bijection of r % 16, so the 16 lanes that read one logical chunk of 16 consecutive
+//           rows hit 16 different chunk positions: row and transposed reads are conflict free;
+//   SW = 3: depends on r % 8 only, so rows r and r + 8 share it and a transposed read of rows
+//           r0 + 8 is the read of rows r0 shifted by a constant (one lane offset fewer per
+//           column block), at the price of a 2-way bank conflict on the row reads.
+// D = 64 (8 chunks per row, two rows per 256-byte bank line): a bijection of (r / 2) % 8 whose
+// top bit follows bit 1 of r (SW = 2), or of (r / 2) % 4 (SW = 3).
+#ifndef LH_SWZ_F
+#define LH_SWZ_F 2  // forward
 #endif
-template <int D>
+#ifndef LH_SWZ_Q
+#define LH_SWZ_Q 2  // dQ
+#endif
+#ifndef LH_SWZ_K
+#define LH_SWZ_K 3  // dK/dV (its register budget has no room for the extra offsets)
+#endif
+template <int D, int SW>
 __device__ __forceinline__ int swz(int r) {
-#if LH_SWZ == 2
-  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
-  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
-#else
-  // depends on r % 8 only, so rows r and r + 8 share it
-  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 1);
-  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 1);
-#endif
+  if constexpr (SW == 2) {
+    if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+    else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+  } else {
+    if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 1);
+    else return (((r >> 1) & 1) << 2) | ((r >> 2) & 1);
+  }
 }
 
 // Byte offsets of one lane inside any swizzled tile (row blocks start at multiples of 16).
@@ -104,19 +120,19 @@ struct LaneOff {
   int trh[D / 32];  // the same 8 rows further (slots 4-7)
 };
 
-template <int D>
+template <int D, int SW>
 __device__ __forceinline__ LaneOff<D> lane_offsets(int lane) {
   constexpr int RB = 2 * D;
   LaneOff<D> o;
   const int h = lane >> 5, r = lane & 31;
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) o.row[kk] = r * RB + (((2 * kk + h) ^ swz<D>(r)) << 4);
+  for (int kk = 0; kk < D / 16; ++kk) o.row[kk] = r * RB + (((2 * kk + h) ^ swz<D, SW>(r)) << 4);
   const int r0 = 4 * h + ((lane & 15) >> 2);
 #pragma unroll
   for (int d = 0; d < D / 32; ++d) {
     const int chunk = 4 * d + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
-    o.trl[d] = r0 * RB + ((chunk ^ swz<D>(r0)) << 4) + 8 * (lane & 1);
-    o.trh[d] = (r0 + 8) * RB + ((chunk ^ swz<D>(r0 + 8)) << 4) + 8 * (lane & 1);
+    o.trl[d] = r0 * RB + ((chunk ^ swz<D, SW>(r0)) << 4) + 8 * (lane & 1);
+    o.trh[d] = (r0 + 8) * RB + ((chunk ^ swz<D, SW>(r0 + 8)) << 4) + 8 * (lane & 1);
   }
   return o;
 }
@@ -155,7 +171,7 @@ __device__ __forceinline__ bf16x8 gld8(const bf16_t* p) { return *reinterpret_ca
 template <int D, int TR, int NW>
 __device__ __forceinline__ constexpr int loads_per_wave() { return (TR * D / 512 + NW - 1) / NW; }
 
-template <int D, int TR, int NW>
+template <int D, int TR, int NW, int SW>
 __device__ __forceinline__ void load_tile(bf16_t* tile, const bf16_t* src, int r0, int S, int w, int lane) {
   constexpr int CPR = D / 8;
   constexpr int BLOCKS = TR * CPR / 64;  // 1 KB blocks of the tile
@@ -166,7 +182,7 @@ __device__ __forceinline__ void load_tile(bf16_t* tile, const bf16_t* src, int r
     if (BLOCKS % NW != 0 && blk >= BLOCKS) blk -= BLOCKS;
     const int pos = blk * 64 + lane;
     const int r = pos / CPR;
-    const int c = (pos % CPR) ^ swz<D>(r);
+    const int c = (pos % CPR) ^ swz<D, SW>(r);
     int gr = r0 + r;
     gr = gr < S ? gr : S - 1;
     __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(src + (int64_t)gr * D + c * 8),
@@ -209,6 +225,22 @@ struct SlotLoop<NS, NS> {
   static __device__ __forceinline__ void run(int, int, F&) {}
 };
 
+// Calls f(IC<t % 2>{}, t) for t = begin .. end - 1: a loop over a two-slot ring that may start
+// on either slot.
+template <typename F>
+__device__ __forceinline__ void ring2_loop(int begin, int end, F& f) {
+  int t = begin;
+  if (t < end && (t & 1)) {
+    f(IC<1>{}, t);
+    ++t;
+  }
+  for (; t + 1 < end; t += 2) {
+    f(IC<0>{}, t);
+    f(IC<1>{}, t + 1);
+  }
+  if (t < end) f(IC<0>{}, t);
+}
+
 // Stores a lane's O^T-layout accumulator row (query row q, columns 32 d + 8 g + 4h + 0..3).
 template <int D>
 __device__ __forceinline__ void store_qrow(bf16_t* row, const f32x16* acc, float mul, int h) {
@@ -246,7 +278,7 @@ sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const 
   const bf16_t* Qh = Q + bh * S * D;
   const bf16_t* Kh = K + bh * S * D;
   const bf16_t* Vh = V + bh * S * D;
-  const LaneOff<D> lo = lane_offsets<D>(lane);
+  const LaneOff<D> lo = lane_offsets<D, LH_SWZ_F>(lane);
 
   const int kend = q0 + FQ < S ? q0 + FQ : S;
   const int nkt = (kend + FK - 1) / FK;
@@ -256,8 +288,8 @@ sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const 
   for (int kk = 0; kk < D / 16; ++kk) qreg[kk] = gld8(Qh + (int64_t)qrow * D + 16 * kk + 8 * h);
 #pragma unroll
   for (int t = 0; t < FNS - 1; ++t) {
-    load_tile<D, FK, FW>(Ks[t], Kh, t * FK, S, w, lane);
-    load_tile<D, FK, FW>(Vs[t], Vh, t * FK, S, w, lane);
+    load_tile<D, FK, FW, LH_SWZ_F>(Ks[t], Kh, t * FK, S, w, lane);
+    load_tile<D, FK, FW, LH_SWZ_F>(Vs[t], Vh, t * FK, S, w, lane);
   }
   f32x16 oacc[D / 32];
 #pragma unroll
@@ -268,8 +300,8 @@ sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const 
     constexpr int SL = decltype(slotc)::value;
     constexpr int NX = (SL + FNS - 1) % FNS;  // slot of tile kt + FNS - 1 (tile kt - 1's)
     sync_tiles<(FNS - 2) * LPT>();  // tile kt landed in every wave; tile kt - 1 is done
-    load_tile<D, FK, FW>(Ks[NX], Kh, (kt + FNS - 1) * FK, S, w, lane);
-    load_tile<D, FK, FW>(Vs[NX], Vh, (kt + FNS - 1) * FK, S, w, lane);
+    load_tile<D, FK, FW, LH_SWZ_F>(Ks[NX], Kh, (kt + FNS - 1) * FK, S, w, lane);
+    load_tile<D, FK, FW, LH_SWZ_F>(Vs[NX], Vh, (kt + FNS - 1) * FK, S, w, lane);
     const int k0 = kt * FK;
     if (qw + 31 < k0) return;  // every key of the tile is in the future of this wave's rows
     const bf16_t* Kt = Ks[SL];
@@ -352,7 +384,7 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
   const bf16_t* Kh = K + bh * S * D;
   const bf16_t* Vh = V + bh * S * D;
   const bf16_t* dOh = dO + bh * S * D;
-  const LaneOff<D> lo = lane_offsets<D>(lane);
+  const LaneOff<D> lo = lane_offsets<D, LH_SWZ_Q>(lane);
 
   const int kend = q0 + BQ < S ? q0 + BQ : S;
   const int nkt = (kend + BK - 1) / BK;
@@ -367,24 +399,27 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
   const float dlt = myq < S ? DELTA[bh * S + myq] : 0.0f;
 #pragma unroll
   for (int t = 0; t < QNS - 1; ++t) {
-    load_tile<D, BK, QW>(Ks[t], Kh, t * BK, S, w, lane);
-    load_tile<D, BK, QW>(Vs[t], Vh, t * BK, S, w, lane);
+    load_tile<D, BK, QW, LH_SWZ_Q>(Ks[t], Kh, t * BK, S, w, lane);
+    load_tile<D, BK, QW, LH_SWZ_Q>(Vs[t], Vh, t * BK, S, w, lane);
   }
   f32x16 dqacc[D / 32];
 #pragma unroll
   for (int d = 0; d < D / 32; ++d) dqacc[d] = f32x16{};
 
-  auto step = [&](auto slotc, int kt) {
+  // Key tiles before q0 hold no key after any row of the block: no mask. Only the last
+  // BQ / BK tiles (the diagonal band) run the masked body.
+  static_assert(QNS == 2, "the masked / unmasked split runs a two-slot ring");
+  auto step = [&](auto slotc, auto maskc, int kt) __attribute__((always_inline)) {
     constexpr int SL = decltype(slotc)::value;
+    constexpr bool MASK = decltype(maskc)::value != 0;
     constexpr int NX = (SL + QNS - 1) % QNS;
     sync_tiles<(QNS - 2) * LPT>();
-    load_tile<D, BK, QW>(Ks[NX], Kh, (kt + QNS - 1) * BK, S, w, lane);
-    load_tile<D, BK, QW>(Vs[NX], Vh, (kt + QNS - 1) * BK, S, w, lane);
+    load_tile<D, BK, QW, LH_SWZ_Q>(Ks[NX], Kh, (kt + QNS - 1) * BK, S, w, lane);
+    load_tile<D, BK, QW, LH_SWZ_Q>(Vs[NX], Vh, (kt + QNS - 1) * BK, S, w, lane);
     const int k0 = kt * BK;
     if (qw + 31 < k0) return;
     const bf16_t* Kt = Ks[SL];
     const bf16_t* Vt = Vs[SL];
-    const bool diag = k0 + BK - 1 > qw;
 #pragma unroll
     for (int kb = 0; kb < BK / 32; ++kb) {
       f32x16 sacc = f32x16{}, pacc = f32x16{};
@@ -400,7 +435,7 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
         for (int t = 0; t < 8; ++t) {
           const int i = 8 * u + t;
           float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[i], sl2, -lse2));
-          if (diag && k0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3) > myq) pv = 0.0f;
+          if (MASK && k0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3) > myq) pv = 0.0f;
           f[t] = pv * (pacc[i] - dlt);
         }
         const bf16x8 db = cvt8(f);
@@ -411,7 +446,11 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
       }
     }
   };
-  for (int t0 = 0; t0 < nkt; t0 += QNS) SlotLoop<0, QNS>::run(t0, nkt, step);
+  const int nfree = q0 / BK < nkt ? q0 / BK : nkt;  // tiles [0, nfree) need no mask
+  auto plain = [&](auto slotc, int kt) __attribute__((always_inline)) { step(slotc, IC<0>{}, kt); };
+  auto masked = [&](auto slotc, int kt) __attribute__((always_inline)) { step(slotc, IC<1>{}, kt); };
+  ring2_loop(0, nfree, plain);
+  ring2_loop(nfree, nkt, masked);
   if (myq < S) store_qrow<D>(dQ + (bh * S + myq) * D, dqacc, scale, h);
 }
 
@@ -446,14 +485,14 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
   const bf16_t* dOh = dO + bh * S * D;
   const float* Lh = LSE + bh * S;
   const float* Dh = DELTA + bh * S;
-  const LaneOff<D> lo = lane_offsets<D>(lane);
+  const LaneOff<D> lo = lane_offsets<D, LH_SWZ_K>(lane);
 
   const int qstart = (k0 / CQ) * CQ;
   const int nqt = (S - qstart + CQ - 1) / CQ;
   auto stage = [&](auto bufc, int qt0) {
     constexpr int BUF = decltype(bufc)::value;
-    load_tile<D, CQ, KWV>(BUF ? Qs1 : Qs0, Qh, qt0, S, w, lane);
-    load_tile<D, CQ, KWV>(BUF ? dOs1 : dOs0, dOh, qt0, S, w, lane);
+    load_tile<D, CQ, KWV, LH_SWZ_K>(BUF ? Qs1 : Qs0, Qh, qt0, S, w, lane);
+    load_tile<D, CQ, KWV, LH_SWZ_K>(BUF ? dOs1 : dOs0, dOh, qt0, S, w, lane);
     if (tid < CQ) {
       const int q = qt0 + tid;
       (BUF ? ls1 : ls0)[tid] = q < S ? Lh[q] * kLog2e : INFINITY;  // rows past S: P = 0
@@ -464,7 +503,7 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
   // then starts on the same tile and streams the same tiles in step with the others, so the
   // blocks running together on an XCD share each Q / dO tile through its L2.
   const int qlast = qstart + (nqt - 1) * CQ;
-  load_tile<D, CK, KWV>(Kw, Kh, k0, S, w, lane);
+  load_tile<D, CK, KWV, LH_SWZ_K>(Kw, Kh, k0, S, w, lane);
   stage(IC<0>{}, qlast);
 
   const int krow = mykey < S ? mykey : S - 1;
