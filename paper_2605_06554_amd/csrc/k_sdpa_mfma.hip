@@ -470,7 +470,9 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
                    const bf16_t* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ DELTA,
                    bf16_t* __restrict__ dK, bf16_t* __restrict__ dV, int S, float sl2, float scale) {
   constexpr int RB = 2 * D;
-  __shared__ __align__(16) bf16_t Qs0[CQ * D], Qs1[CQ * D], dOs0[CQ * D], dOs1[CQ * D];
+  // The query tiles get the larger alignment so that they are laid out first, inside the first
+  // 64 KB, where a tile's base folds into the 16-bit immediate offset of the LDS reads.
+  __shared__ __align__(64) bf16_t Qs0[CQ * D], Qs1[CQ * D], dOs0[CQ * D], dOs1[CQ * D];
   __shared__ __align__(16) float ls0[CQ], ls1[CQ], ds0[CQ], ds1[CQ];
   __shared__ __align__(16) bf16_t Kw[CK * D];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -489,7 +491,7 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
 
   const int qstart = (k0 / CQ) * CQ;
   const int nqt = (S - qstart + CQ - 1) / CQ;
-  auto stage = [&](auto bufc, int qt0) {
+  auto stage = [&](auto bufc, int qt0) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value;
     load_tile<D, CQ, KWV, LH_SWZ_K>(BUF ? Qs1 : Qs0, Qh, qt0, S, w, lane);
     load_tile<D, CQ, KWV, LH_SWZ_K>(BUF ? dOs1 : dOs0, dOh, qt0, S, w, lane);
@@ -514,8 +516,9 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
 #pragma unroll
   for (int d = 0; d < D / 32; ++d) dkacc[d] = dvacc[d] = f32x16{};
 
-  auto tile = [&](auto bufc, int it) {
+  auto tile = [&](auto bufc, auto maskc, int it) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value;
+    constexpr bool MASK = decltype(maskc)::value != 0;
     const bf16_t* Qt = BUF ? Qs1 : Qs0;
     const bf16_t* dOt = BUF ? dOs1 : dOs0;
     const float* lt = BUF ? ls1 : ls0;
@@ -524,9 +527,11 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
     sync_tiles<0>();  // this tile (and its lse / Delta) landed; the other slot is free
     if (it + 1 < nqt) stage(IC<BUF ^ 1>{}, qt0 - CQ);
     if (qt0 + CQ - 1 < kw || kw >= S) return;  // every query of the tile precedes this wave's keys
-    const bool diag = qt0 < kw + 31;
 #pragma unroll
     for (int qb = 0; qb < CQ / 32; ++qb) {
+      // causal mask: element i holds query row qt0 + 32 qb + 4h + c_i, c_i = 8 (i / 4) + i % 4, so
+      // P = 0 exactly where c_i < t (t < 0 on every tile after this wave's diagonal one)
+      const int tmask = mykey - qt0 - 32 * qb - 4 * h;
       // the dP accumulator starts at -Delta (stored negated), so it ends as dP - Delta
       f32x16 sacc = f32x16{}, pacc;
 #pragma unroll
@@ -552,7 +557,7 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
           for (int j = 0; j < 4; ++j) {
             const int i = 8 * u + 4 * g + j;
             float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[i], sl2, -lv[j]));
-            if (diag && mykey > qt0 + qg + j) pv = 0.0f;
+            if (MASK && 8 * (i >> 2) + (i & 3) < tmask) pv = 0.0f;
             pf[4 * g + j] = pv;
             df[4 * g + j] = pv * pacc[i];
           }
@@ -570,10 +575,13 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
       }
     }
   };
-  for (int it = 0; it < nqt; it += 2) {
-    tile(IC<0>{}, it);
-    if (it + 1 < nqt) tile(IC<1>{}, it + 1);
-  }
+  // Query tiles at or after k0 + CK hold no query before any key of the block: no mask. Only the
+  // last CK / CQ tiles visited (the diagonal band) run the masked body.
+  const int nfree = nqt > CK / CQ ? nqt - CK / CQ : 0;
+  auto plain = [&](auto bufc, int it) __attribute__((always_inline)) { tile(bufc, IC<0>{}, it); };
+  auto masked = [&](auto bufc, int it) __attribute__((always_inline)) { tile(bufc, IC<1>{}, it); };
+  ring2_loop(0, nfree, plain);
+  ring2_loop(nfree, nqt, masked);
   // C layout: row = key kw + 8(i/4) + 4h + i%4, column 32 d + lane % 32
 #pragma unroll
   for (int d = 0; d < D / 32; ++d)
