@@ -12,8 +12,9 @@
 // for the data this path sees, so the stored mean is the correctly rounded exact mean.
 //
 // Scores (Q and K only): rows are staged through LDS so that one thread computes one row's
-// squared norm sequentially (c ascending, fp64), takes the correctly rounded fp64 sqrt and
-// rounds to fp32. One thread per head then max-pools the level-0 scores up the levels.
+// squared norm sequentially (c ascending, fp64; 16-byte LDS reads), takes the correctly rounded
+// fp64 sqrt and rounds to fp32. One thread per head then max-pools the level-0 scores up the
+// levels.
 #include "lh_common.h"
 
 namespace lh {
@@ -90,7 +91,9 @@ __global__ void __launch_bounds__(256) pool_score_kernel(PoolArgs a) {
   const bool any_score = a.t[0].s != nullptr || a.t[1].s != nullptr || a.t[2].s != nullptr;
 
   // LDS: staged rows [RB][HW][D + pad] of T, then level-0 scores [RB][HW].
-  const int rowT = D + 8 / (int)sizeof(T);  // +8 bytes keeps the per-row norm reads conflict-free
+  // rows padded by 16 bytes: 16-byte aligned, and the norm threads (one row each, consecutive
+  // rows) read 16-byte chunks without bank conflicts
+  const int rowT = D + 16 / (int)sizeof(T);
   T* tile = reinterpret_cast<T*>(smem);
   float* nrm = reinterpret_cast<float*>(smem + (size_t)kPoolRB * a.HW * rowT * sizeof(T));
 
@@ -202,9 +205,21 @@ __global__ void __launch_bounds__(256) pool_score_kernel(PoolArgs a) {
         const int H2 = t2i == 0 ? t0.H : t2i == 1 ? t1.H : t2.H;
         const T* row = tile + ((size_t)r * a.HW + hh) * rowT;
         double s2 = 0.0;
-        for (int c = 0; c < D; ++c) {
-          const double tv = (double)Elem<T>::load(row + c);
-          s2 += tv * tv;
+        for (int c = 0; c < D; c += CH) {  // 16-byte reads, elements in ascending order
+          const u32x4 w4 = *reinterpret_cast<const u32x4*>(row + c);
+          const uint32_t u[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if constexpr (sizeof(T) == 2) {
+              const double lo = (double)__uint_as_float(u[e] << 16);
+              const double hi = (double)__uint_as_float(u[e] & 0xffff0000u);
+              s2 += lo * lo;  // squares of bf16 values are exact in fp64
+              s2 += hi * hi;
+            } else {
+              const double x = (double)__uint_as_float(u[e]);
+              s2 += x * x;  // squares of fp32 values are exact in fp64
+            }
+          }
         }
         const float sc = (float)sqrt(s2);
         nrm[r * a.HW + hh] = sc;
@@ -270,7 +285,7 @@ static hipError_t launch_T(const LhShape& s, PoolArgs& a, hipStream_t st) {
   dim3 grid((unsigned)((s.N + W - 1) / W), (unsigned)((a.nslots + a.HW - 1) / a.HW), (unsigned)s.B);
   dim3 block((unsigned)(a.HW * CPR));
   const bool score = a.t[0].s || a.t[1].s || a.t[2].s;
-  const int rowT = s.D + 8 / (int)sizeof(T);
+  const int rowT = s.D + 16 / (int)sizeof(T);
   size_t shm = score ? (size_t)kPoolRB * a.HW * rowT * sizeof(T) + (size_t)kPoolRB * a.HW * sizeof(float) : 0;
   switch (s.L) {
     case 1: launch_L<T, 1>(a, grid, block, shm, st); break;
