@@ -171,11 +171,12 @@ __device__ __forceinline__ bf16x8 gld8(const bf16_t* p) { return *reinterpret_ca
 template <int D, int TR, int NW>
 __device__ __forceinline__ constexpr int loads_per_wave() { return (TR * D / 512 + NW - 1) / NW; }
 
-template <int D, int TR, int NW, int SW>
-__device__ __forceinline__ void load_tile(bf16_t* tile, const bf16_t* src, int r0, int S, int w, int lane) {
+template <int D, int TR, int NW, int SW, bool CLAMP>
+__device__ __forceinline__ void load_tile_rows(bf16_t* tile, const bf16_t* src, int r0, int S, int w, int lane) {
   constexpr int CPR = D / 8;
   constexpr int BLOCKS = TR * CPR / 64;  // 1 KB blocks of the tile
   static_assert(BLOCKS * 64 == TR * CPR, "a tile is a whole number of 1 KB blocks");
+  const char* base = reinterpret_cast<const char*>(src + (int64_t)r0 * D);
 #pragma unroll
   for (int j = 0; j < loads_per_wave<D, TR, NW>(); ++j) {
     int blk = j * NW + w;
@@ -183,11 +184,24 @@ __device__ __forceinline__ void load_tile(bf16_t* tile, const bf16_t* src, int r
     const int pos = blk * 64 + lane;
     const int r = pos / CPR;
     const int c = (pos % CPR) ^ swz<D, SW>(r);
-    int gr = r0 + r;
-    gr = gr < S ? gr : S - 1;
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(src + (int64_t)gr * D + c * 8),
+    const char* g;
+    if constexpr (CLAMP) {
+      const int gr = r0 + r < S ? r0 + r : S - 1;
+      g = reinterpret_cast<const char*>(src + (int64_t)gr * D + c * 8);
+    } else {
+      g = base + (uint32_t)((r * D + c * 8) * 2);
+    }
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
                                      (__attribute__((address_space(3))) void*)(tile + blk * 512), 16, 0, 0);
   }
+}
+
+// r0 and w are uniform: a tile that lies inside the matrix is one scalar base address plus a
+// fixed 32-bit offset per lane; only a tile that crosses row S clamps row by row.
+template <int D, int TR, int NW, int SW>
+__device__ __forceinline__ void load_tile(bf16_t* tile, const bf16_t* src, int r0, int S, int w, int lane) {
+  if (r0 + TR <= S) load_tile_rows<D, TR, NW, SW, false>(tile, src, r0, S, w, lane);
+  else load_tile_rows<D, TR, NW, SW, true>(tile, src, r0, S, w, lane);
 }
 
 // Waits until at most N of this wave's vector-memory loads are outstanding and every LDS
@@ -268,7 +282,7 @@ sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const 
   static_assert(FNS >= 2 && FNS <= 4, "ring of 2 to 4 slots");
   LH_RING(bf16_t, Ks, FK * D);
   LH_RING(bf16_t, Vs, FK * D);
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, r32 = lane & 31;
   const int64_t bh = blockIdx.y;
   const int nqt = (S + FQ - 1) / FQ;
@@ -373,7 +387,7 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
   static_assert(QNS >= 2 && QNS <= 4, "ring of 2 to 4 slots");
   LH_RING(bf16_t, Ks, BK * D);
   LH_RING(bf16_t, Vs, BK * D);
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, r32 = lane & 31;
   const int64_t bh = blockIdx.y;
   const int nqt = (S + BQ - 1) / BQ;
@@ -470,12 +484,13 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
                    const bf16_t* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ DELTA,
                    bf16_t* __restrict__ dK, bf16_t* __restrict__ dV, int S, float sl2, float scale) {
   constexpr int RB = 2 * D;
-  // The query tiles get the larger alignment so that they are laid out first, inside the first
-  // 64 KB, where a tile's base folds into the 16-bit immediate offset of the LDS reads.
+  // LDS is laid out by decreasing alignment: the lse / Delta rows (1 KB) first, then the query
+  // tiles, so that both sit inside the first 64 KB, where a base address folds into the 16-bit
+  // immediate offset of the LDS reads (the deepest tile read ends below 63 KB); K comes last.
+  __shared__ __align__(128) float ls0[CQ], ls1[CQ], ds0[CQ], ds1[CQ];
   __shared__ __align__(64) bf16_t Qs0[CQ * D], Qs1[CQ * D], dOs0[CQ * D], dOs1[CQ * D];
-  __shared__ __align__(16) float ls0[CQ], ls1[CQ], ds0[CQ], ds1[CQ];
   __shared__ __align__(16) bf16_t Kw[CK * D];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, r32 = lane & 31;
   const int64_t bh = blockIdx.y;
   const int k0 = (int)blockIdx.x * CK;  // early keys see the most queries: launched first
