@@ -24,6 +24,10 @@
 // give every XCD one contiguous eighth of the runs.
 #include "lh_common.h"
 
+#ifndef LH_GBWD_GB
+#define LH_GBWD_GB 4  // gather+pool adjoint: query heads whose loads are issued together
+#endif
+
 namespace lh {
 
 // With gridDim.x a multiple of 8, blockIdx.x % 8 is the XCD of the workgroup; XCD x gets the
@@ -124,6 +128,8 @@ struct RunArgs {
   int32_t pshift;                     // log2 p when p is a power of two, else -1
   int32_t pw[16];                     // p^l
   int32_t off[17];                    // flattened id of entry (l, 0)
+  int32_t nrow[16];                   // N / p^l
+  int32_t vec_slots;                  // Ptot % 4 == 0: a head's slot row is 16-byte aligned
   float inv[16];                      // 1 / p^l
 };
 
@@ -286,6 +292,333 @@ __global__ void __launch_bounds__(256) gather_bwd_kernel(RunArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- long runs (p = 2, 4)
+// A thread handles RL = P^TT positions (16 for p = 4, 8 for p = 2). Levels l >= TT have one
+// entry per run, levels 1 <= l < TT one entry per sub-run of p^l positions, level 0 one per
+// position. When the run lies inside level 0, its level-0 slots are read as 16-byte vectors.
+// Every slot and then every row of the run is loaded before the sums, which keep the order of
+// the runs of p above (levels L-1 .. 1, then level 0), so the results are the same bits.
+constexpr int ipow(int p, int e) { return e == 0 ? 1 : p * ipow(p, e - 1); }
+// index of the first level-l sub-run entry in the flattened list of levels 1 .. l-1
+constexpr int sub_off(int P, int TT, int l) {
+  int s = 0;
+  for (int x = 1; x < l; ++x) s += ipow(P, TT - x);
+  return s;
+}
+
+// Level-0 slots of positions j0 .. j0 + RL - 1 (-1 outside [0, N)). Positions j0 + SH .. start
+// at a multiple of 4 (SH = 1 for the scatter's shifted runs). When the 4-aligned block
+// [j0 + SH, j0 + SH + RL) lies inside level 0 it is read as RL / 4 16-byte vectors (the last SH
+// values unused) and the first SH positions one by one.
+template <int RL, int SH>
+__device__ __forceinline__ void load_level0_slots(const RunArgs& a, const int32_t* sl, int32_t j0, int32_t* m0) {
+  const int32_t base = j0 + SH;
+  if (a.vec_slots && j0 >= 0 && base + RL <= a.N) {
+    int32_t t[RL];
+#pragma unroll
+    for (int q = 0; q < RL / 4; ++q) {
+      const int4 w = *reinterpret_cast<const int4*>(sl + base + 4 * q);
+      t[4 * q] = w.x, t[4 * q + 1] = w.y, t[4 * q + 2] = w.z, t[4 * q + 3] = w.w;
+    }
+#pragma unroll
+    for (int r = 0; r < SH; ++r) m0[r] = sl[j0 + r];
+#pragma unroll
+    for (int r = SH; r < RL; ++r) m0[r] = t[r - SH];
+  } else {
+#pragma unroll
+    for (int r = 0; r < RL; ++r) {
+      const int32_t j = j0 + r;
+      m0[r] = (j >= 0 && j < a.N) ? sl[j] : -1;
+    }
+  }
+}
+
+__device__ __forceinline__ u32x4 load_entry_row(const void* src, int32_t m, int32_t S, int D, int esz) {
+  return (uint32_t)m < (uint32_t)S
+             ? load_raw(reinterpret_cast<const char*>(src) + (int64_t)m * D * esz)
+             : u32x4{0, 0, 0, 0};
+}
+
+// Scatter over runs c of RL positions j = c RL + r - 1.
+template <typename T, int L, int P, int TT>
+__global__ void __launch_bounds__(256) scatter_long_kernel(RunArgs a) {
+  constexpr int CH = 16 / sizeof(T);
+  constexpr int RL = ipow(P, TT);
+  constexpr int LS = TT < L ? TT : L;  // levels 1 .. LS-1 change inside the run
+  constexpr int NSUB = sub_off(P, TT, LS);
+  constexpr int NSH = L - LS;  // levels LS .. L-1: one entry per run
+  const uint32_t c = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int hc = blockIdx.y * blockDim.x + threadIdx.x;
+  if (c >= (uint32_t)a.nruns || hc >= a.HC) return;
+  const int hq = hc >> a.cpr_shift, cc = hc & ((1 << a.cpr_shift) - 1);
+  const int64_t b = blockIdx.z;
+  const int64_t bh = b * a.Hq + hq;
+  const int32_t* sl = a.slot + bh * a.Ptot;
+  const T* src = reinterpret_cast<const T*>(a.src) + bh * a.S * a.D + cc * CH;
+  const int32_t j0 = (int32_t)(c * RL) - 1;
+  int32_t msh[NSH > 0 ? NSH : 1], msub[NSUB > 0 ? NSUB : 1], m0[RL];
+#pragma unroll
+  for (int l = LS; l < L; ++l) {  // entry floor((j + 1) / p^l) - 1 = floor(c / p^(l - TT)) - 1
+    const int32_t i = (int32_t)(c / (uint32_t)ipow(P, l - TT)) - 1;
+    msh[l - LS] = (i >= 0 && i < a.nrow[l]) ? sl[a.off[l] + i] : -1;
+  }
+#pragma unroll
+  for (int l = 1; l < LS; ++l)  // sub-run s: entry c p^(TT-l) + s - 1
+#pragma unroll
+    for (int s2 = 0; s2 < ipow(P, TT - l); ++s2) {
+      const int32_t i = (int32_t)(c * ipow(P, TT - l)) + s2 - 1;
+      msub[sub_off(P, TT, l) + s2] = (i >= 0 && i < a.nrow[l]) ? sl[a.off[l] + i] : -1;
+    }
+  load_level0_slots<RL, 1>(a, sl, j0, m0);
+  u32x4 vsh[NSH > 0 ? NSH : 1], vsub[NSUB > 0 ? NSUB : 1], v0[RL];
+#pragma unroll
+  for (int x = 0; x < NSH; ++x) vsh[x] = load_entry_row(src, msh[x], a.S, a.D, sizeof(T));
+#pragma unroll
+  for (int x = 0; x < NSUB; ++x) vsub[x] = load_entry_row(src, msub[x], a.S, a.D, sizeof(T));
+#pragma unroll
+  for (int r = 0; r < RL; ++r) v0[r] = load_entry_row(src, m0[r], a.S, a.D, sizeof(T));
+  float acc[CH];
+#pragma unroll
+  for (int e = 0; e < CH; ++e) acc[e] = 0.0f;
+#pragma unroll
+  for (int l = L - 1; l >= LS; --l) add_chunk<T>(acc, vsh[l - LS]);
+  T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.Hq + hq) * (int64_t)a.D + cc * CH;
+  const int64_t dstride = (int64_t)a.Hq * a.D;
+#pragma unroll
+  for (int r = 0; r < RL; ++r) {
+    const int32_t j = j0 + r;
+    if (j < 0 || j >= a.N) continue;
+    float o[CH];
+#pragma unroll
+    for (int e = 0; e < CH; ++e) o[e] = acc[e];
+#pragma unroll
+    for (int l = LS - 1; l >= 1; --l) add_chunk<T>(o, vsub[sub_off(P, TT, l) + r / ipow(P, l)]);
+    add_chunk<T>(o, v0[r]);
+    store_chunk<T>(dst + (int64_t)j * dstride, o);
+  }
+}
+
+// Gather + pool adjoint of one query head per output head (dQ) over runs c of RL positions
+// j = c RL + r.
+template <typename T, int L, int P, int TT>
+__global__ void __launch_bounds__(256) gather_bwd_long_kernel(RunArgs a) {
+  constexpr int CH = 16 / sizeof(T);
+  constexpr int RL = ipow(P, TT);
+  constexpr int LS = TT < L ? TT : L;
+  constexpr int NSUB = sub_off(P, TT, LS);
+  constexpr int NSH = L - LS;
+  const uint32_t c = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int hc = blockIdx.y * blockDim.x + threadIdx.x;
+  if (c >= (uint32_t)a.nruns || hc >= a.HC) return;
+  const int h = hc >> a.cpr_shift, cc = hc & ((1 << a.cpr_shift) - 1);
+  const int64_t b = blockIdx.z;
+  const int64_t bh = b * a.Hq + h;
+  const int32_t* sl = a.slot + bh * a.Ptot;
+  const T* src = reinterpret_cast<const T*>(a.src) + bh * a.S * a.D + cc * CH;
+  const int32_t j0 = (int32_t)(c * RL);
+  int32_t msh[NSH > 0 ? NSH : 1], msub[NSUB > 0 ? NSUB : 1], m0[RL];
+#pragma unroll
+  for (int l = LS; l < L; ++l) {  // entry floor(j / p^l) = floor(c / p^(l - TT))
+    const int32_t i = (int32_t)(c / (uint32_t)ipow(P, l - TT));
+    msh[l - LS] = i < a.nrow[l] ? sl[a.off[l] + i] : -1;
+  }
+#pragma unroll
+  for (int l = 1; l < LS; ++l)
+#pragma unroll
+    for (int s2 = 0; s2 < ipow(P, TT - l); ++s2) {
+      const int32_t i = (int32_t)(c * ipow(P, TT - l)) + s2;
+      msub[sub_off(P, TT, l) + s2] = i < a.nrow[l] ? sl[a.off[l] + i] : -1;
+    }
+  load_level0_slots<RL, 0>(a, sl, j0, m0);
+  u32x4 vsh[NSH > 0 ? NSH : 1], vsub[NSUB > 0 ? NSUB : 1], v0[RL];
+#pragma unroll
+  for (int x = 0; x < NSH; ++x) vsh[x] = load_entry_row(src, msh[x], a.S, a.D, sizeof(T));
+#pragma unroll
+  for (int x = 0; x < NSUB; ++x) vsub[x] = load_entry_row(src, msub[x], a.S, a.D, sizeof(T));
+#pragma unroll
+  for (int r = 0; r < RL; ++r) v0[r] = load_entry_row(src, m0[r], a.S, a.D, sizeof(T));
+  float acc[CH];
+#pragma unroll
+  for (int e = 0; e < CH; ++e) acc[e] = 0.0f;
+#pragma unroll
+  for (int l = L - 1; l >= LS; --l) add_chunk_scaled<T>(acc, vsh[l - LS], a.inv[l]);
+  T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.H + h) * (int64_t)a.D + cc * CH;
+  const int64_t dstride = (int64_t)a.H * a.D;
+#pragma unroll
+  for (int r = 0; r < RL; ++r) {
+    const int32_t j = j0 + r;
+    if (j >= a.N) continue;
+    float o[CH], fine[CH];
+#pragma unroll
+    for (int e = 0; e < CH; ++e) o[e] = acc[e], fine[e] = 0.0f;
+#pragma unroll
+    for (int l = LS - 1; l >= 1; --l) add_chunk_scaled<T>(o, vsub[sub_off(P, TT, l) + r / ipow(P, l)], a.inv[l]);
+    add_chunk<T>(fine, v0[r]);
+#pragma unroll
+    for (int e = 0; e < CH; ++e) o[e] = o[e] + fine[e];
+    store_chunk<T>(dst + (int64_t)j * dstride, o);
+  }
+}
+
+// Gather + pool adjoint summed over the Gs query heads of a group (dK, dV), runs of p <= 4
+// positions: the slots and then the rows of GB heads at a time are loaded before their sums,
+// which keep the order of gather_bwd_kernel.
+template <typename T, int L, int GB>
+__global__ void __launch_bounds__(256) gather_bwd_group_kernel(RunArgs a) {
+  constexpr int CH = 16 / sizeof(T);
+  constexpr int PU = 4;
+  constexpr int LA = L > 1 ? L : 2;
+  const uint32_t c = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int hc = blockIdx.y * blockDim.x + threadIdx.x;
+  if (c >= (uint32_t)a.nruns || hc >= a.HC) return;
+  const int h = hc >> a.cpr_shift, cc = hc & ((1 << a.cpr_shift) - 1);
+  const int64_t b = blockIdx.z;
+  const int32_t jbase = (int32_t)(c * (uint32_t)a.run);
+  int32_t ent[LA];
+#pragma unroll
+  for (int l = 1; l < L; ++l) ent[l] = a.off[l] + run_entry(a, c, l);
+  float acc[CH], fine[PU][CH];
+#pragma unroll
+  for (int e = 0; e < CH; ++e) acc[e] = 0.0f;
+#pragma unroll
+  for (int r = 0; r < PU; ++r)
+#pragma unroll
+    for (int e = 0; e < CH; ++e) fine[r][e] = 0.0f;
+  for (int g0 = 0; g0 < a.Gs; g0 += GB) {
+    int32_t m[GB][LA], m0[GB][PU];
+#pragma unroll
+    for (int gg = 0; gg < GB; ++gg) {
+      const bool live = g0 + gg < a.Gs;
+      const int32_t* sl = a.slot + (b * a.Hq + (int64_t)h * a.Gs + g0 + gg) * a.Ptot;
+#pragma unroll
+      for (int l = L - 1; l >= 1; --l) m[gg][l] = live ? sl[ent[l]] : -1;
+#pragma unroll
+      for (int r = 0; r < PU; ++r) m0[gg][r] = (live && r < a.run) ? sl[jbase + r] : -1;
+    }
+    u32x4 v[GB][LA], v0[GB][PU];
+#pragma unroll
+    for (int gg = 0; gg < GB; ++gg) {
+      const T* src = reinterpret_cast<const T*>(a.src) +
+                     (b * a.Hq + (int64_t)h * a.Gs + g0 + gg) * a.S * a.D + cc * CH;
+#pragma unroll
+      for (int l = L - 1; l >= 1; --l) v[gg][l] = load_entry_row(src, m[gg][l], a.S, a.D, sizeof(T));
+#pragma unroll
+      for (int r = 0; r < PU; ++r) v0[gg][r] = load_entry_row(src, m0[gg][r], a.S, a.D, sizeof(T));
+    }
+#pragma unroll
+    for (int gg = 0; gg < GB; ++gg) {
+      if (g0 + gg >= a.Gs) break;
+#pragma unroll
+      for (int l = L - 1; l >= 1; --l) add_chunk_scaled<T>(acc, v[gg][l], a.inv[l]);
+#pragma unroll
+      for (int r = 0; r < PU; ++r) add_chunk<T>(fine[r], v0[gg][r]);
+    }
+  }
+  T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.H + h) * (int64_t)a.D + cc * CH;
+  const int64_t dstride = (int64_t)a.H * a.D;
+#pragma unroll
+  for (int r = 0; r < PU; ++r) {
+    if (r < a.run) {
+      float o[CH];
+#pragma unroll
+      for (int e = 0; e < CH; ++e) o[e] = acc[e] + fine[r][e];
+      store_chunk<T>(dst + (int64_t)(jbase + r) * dstride, o);
+    }
+  }
+}
+
+// Gather + pool adjoint summed over the Gs query heads of a group (dK, dV) for p a power of two:
+// a thread handles RH = 2^RHL positions j = c RH + r (RH a multiple of p). A level-l entry is
+// shared by the run when p^l >= RH; otherwise the run holds RH / p^l of them. Heads are visited
+// in order with the next head's slots loaded while the current head's rows are in flight. The
+// sums keep the order of gather_bwd_kernel: for each window of p positions, levels L-1 .. 1 of
+// every head in turn; per position, level 0 of every head in turn; one rounding.
+template <int PL, int RHL, int L>
+struct GroupRun {
+  static constexpr int RH = 1 << RHL;
+  static constexpr int P = 1 << PL;
+  static constexpr int NW = RH / P;  // level-1 windows per run
+  // entries of level l in the run (1 when shared)
+  static constexpr int cnt(int l) { return l * PL >= RHL ? 1 : 1 << (RHL - l * PL); }
+  static constexpr int base(int l) {  // index of level l's first entry in the flattened list
+    int s = 0;
+    for (int x = 1; x < l; ++x) s += cnt(x);
+    return s;
+  }
+  static constexpr int NE = base(L) + RH;  // coarse entries, then RH level-0 entries
+};
+
+template <typename T, int L, int PL, int RHL>
+__global__ void __launch_bounds__(256) gather_bwd_group_long_kernel(RunArgs a) {
+  using G = GroupRun<PL, RHL, L>;
+  constexpr int CH = 16 / sizeof(T);
+  constexpr int RH = G::RH, NW = G::NW, NE = G::NE, NC = G::base(L);
+  const uint32_t c = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int hc = blockIdx.y * blockDim.x + threadIdx.x;
+  if (c >= (uint32_t)a.nruns || hc >= a.HC) return;
+  const int h = hc >> a.cpr_shift, cc = hc & ((1 << a.cpr_shift) - 1);
+  const int64_t b = blockIdx.z;
+  const int32_t j0 = (int32_t)(c * RH);
+  // flattened slot indices (into one head's slot row) of the run's entries; -1: none
+  int32_t sidx[NE];
+#pragma unroll
+  for (int l = 1; l < L; ++l)
+#pragma unroll
+    for (int e = 0; e < G::cnt(l); ++e) {
+      // entry floor(j / p^l) for the first position of sub-run e
+      const int32_t i = G::cnt(l) == 1 ? (int32_t)((uint32_t)j0 >> (l * PL)) : (j0 >> (l * PL)) + e;
+      sidx[G::base(l) + e] = i < a.nrow[l] ? a.off[l] + i : -1;
+    }
+#pragma unroll
+  for (int r = 0; r < RH; ++r) sidx[NC + r] = j0 + r < a.N ? j0 + r : -1;
+  const int64_t bhq0 = b * a.Hq + (int64_t)h * a.Gs;
+  auto load_slots = [&](int g, int32_t* m) __attribute__((always_inline)) {
+    const int32_t* sl = a.slot + (bhq0 + g) * a.Ptot;
+#pragma unroll
+    for (int e = 0; e < NE; ++e) m[e] = sidx[e] >= 0 ? sl[sidx[e]] : -1;
+  };
+  float acc[NW][CH], fine[RH][CH];
+#pragma unroll
+  for (int w = 0; w < NW; ++w)
+#pragma unroll
+    for (int e = 0; e < CH; ++e) acc[w][e] = 0.0f;
+#pragma unroll
+  for (int r = 0; r < RH; ++r)
+#pragma unroll
+    for (int e = 0; e < CH; ++e) fine[r][e] = 0.0f;
+  int32_t m[NE], mn[NE];
+  load_slots(0, m);
+  for (int g = 0; g < a.Gs; ++g) {
+    const T* src = reinterpret_cast<const T*>(a.src) + (bhq0 + g) * a.S * a.D + cc * CH;
+    u32x4 v[NE];
+#pragma unroll
+    for (int e = 0; e < NE; ++e) v[e] = load_entry_row(src, m[e], a.S, a.D, sizeof(T));
+    if (g + 1 < a.Gs) load_slots(g + 1, mn);
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+#pragma unroll
+      for (int l = L - 1; l >= 1; --l) {
+        // the level-l entry of window w (windows of p positions nest in sub-runs of p^l)
+        const int e = G::cnt(l) == 1 ? 0 : (w * G::P) >> (l * PL);
+        add_chunk_scaled<T>(acc[w], v[G::base(l) + e], a.inv[l]);
+      }
+#pragma unroll
+    for (int r = 0; r < RH; ++r) add_chunk<T>(fine[r], v[NC + r]);
+#pragma unroll
+    for (int e = 0; e < NE; ++e) m[e] = mn[e];
+  }
+  T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.H + h) * (int64_t)a.D + cc * CH;
+  const int64_t dstride = (int64_t)a.H * a.D;
+#pragma unroll
+  for (int r = 0; r < RH; ++r) {
+    if (j0 + r >= a.N) continue;
+    float o[CH];
+#pragma unroll
+    for (int e = 0; e < CH; ++e) o[e] = acc[r / G::P][e] + fine[r][e];
+    store_chunk<T>(dst + (int64_t)(j0 + r) * dstride, o);
+  }
+}
+
 // ---------------------------------------------------------------- scatter_bwd
 
 struct ScatterBwdArgs {
@@ -392,26 +725,64 @@ static int cpr_shift_of(int D, int esize) {
   return s;
 }
 
-template <typename T, int L>
-static void launch_scatter_P(const RunArgs& a, dim3 grid, dim3 block, hipStream_t st) {
-  if (a.run <= 4) hipLaunchKernelGGL((scatter_kernel<T, L, 4>), grid, block, 0, st, a);
-  else hipLaunchKernelGGL((scatter_kernel<T, L, 0>), grid, block, 0, st, a);
+// Long runs of p^2 (p = 4) or p^3 (p = 2) positions for the scatter and for adjoints with one
+// query head per output head; runs of p otherwise.
+static int long_run_tt(const LhShape& s) {
+  if (s.L < 2) return 0;
+  if (s.p == 4) return 2;
+  if (s.p == 2) return 3;
+  return 0;
 }
 
 template <typename T, int L>
-static void launch_gather_bwd_P(const RunArgs& a, dim3 grid, dim3 block, hipStream_t st) {
-  if (a.run <= 4) hipLaunchKernelGGL((gather_bwd_kernel<T, L, 4>), grid, block, 0, st, a);
-  else hipLaunchKernelGGL((gather_bwd_kernel<T, L, 0>), grid, block, 0, st, a);
+static void launch_scatter_P(const LhShape& s, RunArgs a, dim3 grid, dim3 block, hipStream_t st) {
+  const int tt = long_run_tt(s);
+  if (tt) {
+    const int rl = tt == 2 ? 16 : 8;
+    a.nruns = (int32_t)((s.N + rl) / rl);  // j = c rl + r - 1 up to N - 1
+    grid.x = (unsigned)((a.nruns + 7) / 8 * 8);
+    if (tt == 2) hipLaunchKernelGGL((scatter_long_kernel<T, L, 4, 2>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((scatter_long_kernel<T, L, 2, 3>), grid, block, 0, st, a);
+  } else if (a.run <= 4) {
+    hipLaunchKernelGGL((scatter_kernel<T, L, 4>), grid, block, 0, st, a);
+  } else {
+    hipLaunchKernelGGL((scatter_kernel<T, L, 0>), grid, block, 0, st, a);
+  }
+}
+
+template <typename T, int L>
+static void launch_gather_bwd_P(const LhShape& s, RunArgs a, dim3 grid, dim3 block, hipStream_t st) {
+  const int tt = long_run_tt(s);
+  if (a.Gs == 1 && tt) {
+    const int rl = tt == 2 ? 16 : 8;
+    a.nruns = (int32_t)((s.N + rl - 1) / rl);
+    grid.x = (unsigned)((a.nruns + 7) / 8 * 8);
+    if (tt == 2) hipLaunchKernelGGL((gather_bwd_long_kernel<T, L, 4, 2>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((gather_bwd_long_kernel<T, L, 2, 3>), grid, block, 0, st, a);
+  } else if (a.Gs > 1 && L > 1 && (s.p == 2 || s.p == 4)) {
+    constexpr int RHL = 3;  // runs of 8 positions
+    a.nruns = (int32_t)((s.N + 7) / 8);
+    grid.x = (unsigned)((a.nruns + 7) / 8 * 8);
+    if (s.p == 4) hipLaunchKernelGGL((gather_bwd_group_long_kernel<T, L, 2, RHL>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((gather_bwd_group_long_kernel<T, L, 1, RHL>), grid, block, 0, st, a);
+  } else if (a.Gs > 1 && a.run <= 4) {
+    hipLaunchKernelGGL((gather_bwd_group_kernel<T, L, LH_GBWD_GB>), grid, block, 0, st, a);
+  } else if (a.run <= 4) {
+    hipLaunchKernelGGL((gather_bwd_kernel<T, L, 4>), grid, block, 0, st, a);
+  } else {
+    hipLaunchKernelGGL((gather_bwd_kernel<T, L, 0>), grid, block, 0, st, a);
+  }
 }
 
 template <typename T>
-static void launch_run_kernel(bool scatter, int L, const RunArgs& a, dim3 grid, dim3 block, hipStream_t st) {
+static void launch_run_kernel(bool scatter, const LhShape& s, const RunArgs& a, dim3 grid, dim3 block,
+                              hipStream_t st) {
 #define LH_RUN_CASE(LL)                                            \
   case LL:                                                         \
-    if (scatter) launch_scatter_P<T, LL>(a, grid, block, st);      \
-    else launch_gather_bwd_P<T, LL>(a, grid, block, st);           \
+    if (scatter) launch_scatter_P<T, LL>(s, a, grid, block, st);   \
+    else launch_gather_bwd_P<T, LL>(s, a, grid, block, st);        \
     break;
-  switch (L) {
+  switch (s.L) {
     LH_RUN_CASE(1)
     LH_RUN_CASE(2)
     LH_RUN_CASE(3)
@@ -452,6 +823,8 @@ static RunArgs run_args(const LhShape& s, const void* src, const int32_t* slot, 
     a.inv[l] = l < s.L ? 1.0f / (float)s.pw[l] : 0.0f;
   }
   for (int l = 0; l < 17; ++l) a.off[l] = (int32_t)s.off[l];
+  for (int l = 0; l < 16; ++l) a.nrow[l] = l < s.L ? (int32_t)(s.N / s.pw[l]) : 0;
+  a.vec_slots = (s.Ptot % 4) == 0;
   return a;
 }
 
@@ -530,8 +903,8 @@ hipError_t lh_launch_scatter(const LhShape& s, const void* os, const int32_t* sl
   const RunArgs a = run_args(s, os, slot, o, s.Hq, 1, true);
   dim3 grid, block;
   run_grid(a, (int)s.B, &grid, &block);
-  if (s.dtype == LH_BF16) launch_run_kernel<bf16_t>(true, s.L, a, grid, block, st);
-  else launch_run_kernel<float>(true, s.L, a, grid, block, st);
+  if (s.dtype == LH_BF16) launch_run_kernel<bf16_t>(true, s, a, grid, block, st);
+  else launch_run_kernel<float>(true, s, a, grid, block, st);
   return hipGetLastError();
 }
 
@@ -551,8 +924,8 @@ hipError_t lh_launch_gather_bwd(const LhShape& s, const void* dqs, const void* d
                                which == 0 ? 1 : s.G, false);
     dim3 grid, block;
     run_grid(a, (int)s.B, &grid, &block);
-    if (s.dtype == LH_BF16) launch_run_kernel<bf16_t>(false, s.L, a, grid, block, st);
-    else launch_run_kernel<float>(false, s.L, a, grid, block, st);
+    if (s.dtype == LH_BF16) launch_run_kernel<bf16_t>(false, s, a, grid, block, st);
+    else launch_run_kernel<float>(false, s, a, grid, block, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
