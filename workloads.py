@@ -74,6 +74,10 @@ TEST_CONFIGS = {
     # stratified selection (flag bit 1): levels 2 and 1 rank 4096 and 3000 candidates in chunks
     # of 2048, S = 4096 + 3000 + 3000
     "t_strat": Config("t_strat", 1, 16384, 2, 1, 64, 2, 3, 1500, "bf16", 2006, "spikes", 0.01, flags=2),
+    # L = 2 with N = 4 * 257: the last run of p^2 positions is partial; Ptot = 1285 (odd)
+    "t_l2": Config("t_l2", 1, 1028, 2, 2, 64, 4, 2, 64, "bf16", 2007),
+    # p = 2, L = 5, N = 112: Ptot = 217 (odd), three query heads per KV head
+    "t_g3": Config("t_g3", 1, 112, 3, 1, 64, 2, 5, 5, "bf16", 2008),
 }
 
 
