@@ -99,7 +99,8 @@ enum {
   LH_OP_SELECT = 0,         /* lh_select_topk          */
   LH_OP_SDPA_BWD = 1,       /* lh_sdpa_bwd             */
   LH_OP_ATTENTION_FWD = 2,  /* lh_attention_fwd        */
-  LH_OP_ATTENTION_BWD = 3   /* lh_attention_bwd        */
+  LH_OP_ATTENTION_BWD = 3,  /* lh_attention_bwd and lh_attention_bwd_indexed */
+  LH_OP_ATTENTION_FWD_INDEXED = 4  /* lh_attention_fwd_indexed */
 };
 
 typedef struct {
@@ -217,6 +218,46 @@ lh_status lh_attention_bwd(const lh_problem* pr, const int32_t* idx, const int32
                            const void* qs, const void* ks, const void* vs, const void* os,
                            const float* lse, const void* dout, void* dq, void* dk, void* dv,
                            void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------- gather fused into the SDPA loads ---------------- */
+/* The same computation as the calls above with the gathered rows never materialised
+   (Sec. 3.5, gather equation): the SDPA kernels read row m of Q~, K~, V~ of head (b, hq)
+   straight from pyramid id idx[b,hq,m] of q / qpyr (query head hq) and k, v / kpyr, vpyr
+   (KV head hq / (Hq / Hkv)). Given the same inputs, outputs are bitwise identical to those of
+   lh_gather followed by lh_sdpa_fwd / lh_sdpa_bwd. bf16 only (LH_E_DTYPE otherwise). qpyr,
+   kpyr, vpyr are the pyramid buffers of lh_pyramid_pool ([B,R,H,D], R = Ptot - N); they may be
+   NULL when L = 1. idx must hold pyramid ids in [0, Ptot) as written by lh_select_topk; an id
+   outside that range is clamped into it (no out-of-range read; the row it reads is
+   unspecified). */
+lh_status lh_sdpa_fwd_indexed(const lh_problem* pr, const void* q, const void* k, const void* v,
+                              const void* qpyr, const void* kpyr, const void* vpyr,
+                              const int32_t* idx, void* os, float* lse, void* stream);
+
+/* Gradient of lh_sdpa_fwd_indexed: writes dqs, dks, dvs [B,Hq,S,D] (the gathered-row
+   gradients, as lh_sdpa_bwd). ws: at least lh_workspace_bytes(LH_OP_SDPA_BWD) bytes. */
+lh_status lh_sdpa_bwd_indexed(const lh_problem* pr, const void* q, const void* k, const void* v,
+                              const void* qpyr, const void* kpyr, const void* vpyr,
+                              const int32_t* idx, const void* os, const float* lse,
+                              const void* dos, void* dqs, void* dks, void* dvs, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/* lh_attention_fwd without qs, ks, vs: the caller keeps the pyramid instead (qpyr [B,R,Hq,D],
+   kpyr and vpyr [B,R,Hkv,D]; unused and may be NULL when L = 1), which the backward reads.
+   ws: at least lh_workspace_bytes(LH_OP_ATTENTION_FWD_INDEXED) bytes (scores and selection
+   lists). bf16 only. Outputs are bitwise identical to those of lh_attention_fwd. */
+lh_status lh_attention_fwd_indexed(const lh_problem* pr, const void* q, const void* k,
+                                   const void* v, void* o, int32_t* idx, int32_t* slot,
+                                   void* qpyr, void* kpyr, void* vpyr, void* os, float* lse,
+                                   void* ws, size_t ws_bytes, void* stream);
+
+/* lh_attention_bwd from the state of lh_attention_fwd_indexed (q, k, v and the pyramid in
+   place of qs, ks, vs). ws: at least lh_workspace_bytes(LH_OP_ATTENTION_BWD) bytes. bf16 only.
+   Outputs are bitwise identical to those of lh_attention_bwd. */
+lh_status lh_attention_bwd_indexed(const lh_problem* pr, const void* q, const void* k,
+                                   const void* v, const void* qpyr, const void* kpyr,
+                                   const void* vpyr, const int32_t* idx, const int32_t* slot,
+                                   const void* os, const float* lse, const void* dout, void* dq,
+                                   void* dk, void* dv, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

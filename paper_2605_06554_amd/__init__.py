@@ -15,20 +15,21 @@ import torch
 
 __all__ = [
     "LH_OK", "LH_F32", "LH_BF16", "LH_FLAG_REPLACE_PARENTS", "LH_FLAG_STRATIFIED", "LH_OP_SELECT", "LH_OP_SDPA_BWD",
-    "LH_OP_ATTENTION_FWD", "LH_OP_ATTENTION_BWD", "LighthouseError", "lh_problem", "problem",
+    "LH_OP_ATTENTION_FWD", "LH_OP_ATTENTION_BWD", "LH_OP_ATTENTION_FWD_INDEXED", "LighthouseError", "lh_problem", "problem",
     "lh_check", "lh_level_rows", "lh_level_offset", "lh_pyramid_rows", "lh_subseq_len",
     "lh_workspace_bytes", "lh_status_str", "lh_last_error", "lh_pyramid_pool", "lh_score",
     "lh_pool_score", "lh_select_topk", "lh_gather", "lh_sdpa_fwd", "lh_sdpa_bwd", "lh_scatter",
-    "lh_scatter_bwd", "lh_gather_bwd", "lh_attention_fwd", "lh_attention_bwd", "workspace",
-    "attention_forward",
-    "attention_backward", "library_path", "EXPORTED",
+    "lh_scatter_bwd", "lh_gather_bwd", "lh_attention_fwd", "lh_attention_bwd", "lh_sdpa_fwd_indexed",
+    "lh_sdpa_bwd_indexed", "lh_attention_fwd_indexed", "lh_attention_bwd_indexed", "workspace",
+    "attention_forward", "attention_backward", "attention_forward_indexed", "attention_backward_indexed",
+    "library_path", "EXPORTED",
 ]
 
 LH_OK = 0
 LH_F32, LH_BF16 = 0, 1
 LH_FLAG_REPLACE_PARENTS = 1
 LH_FLAG_STRATIFIED = 2
-LH_OP_SELECT, LH_OP_SDPA_BWD, LH_OP_ATTENTION_FWD, LH_OP_ATTENTION_BWD = 0, 1, 2, 3
+LH_OP_SELECT, LH_OP_SDPA_BWD, LH_OP_ATTENTION_FWD, LH_OP_ATTENTION_BWD, LH_OP_ATTENTION_FWD_INDEXED = 0, 1, 2, 3, 4
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 library_path = os.path.join(_HERE, "liblighthouse.so")
@@ -37,7 +38,8 @@ EXPORTED = [
     "lh_check", "lh_level_rows", "lh_level_offset", "lh_pyramid_rows", "lh_subseq_len",
     "lh_workspace_bytes", "lh_status_str", "lh_last_error", "lh_pyramid_pool", "lh_score",
     "lh_pool_score", "lh_select_topk", "lh_gather", "lh_sdpa_fwd", "lh_sdpa_bwd", "lh_scatter", "lh_scatter_bwd",
-    "lh_gather_bwd", "lh_attention_fwd", "lh_attention_bwd",
+    "lh_gather_bwd", "lh_attention_fwd", "lh_attention_bwd", "lh_sdpa_fwd_indexed", "lh_sdpa_bwd_indexed",
+    "lh_attention_fwd_indexed", "lh_attention_bwd_indexed",
 ]
 
 
@@ -97,6 +99,10 @@ def _load():
         "lh_gather_bwd": (i32, [PR, P, P, P, P, P, P, P, P]),
         "lh_attention_fwd": (i32, [PR, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]),
         "lh_attention_bwd": (i32, [PR, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]),
+        "lh_sdpa_fwd_indexed": (i32, [PR, P, P, P, P, P, P, P, P, P, P]),
+        "lh_sdpa_bwd_indexed": (i32, [PR, P, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]),
+        "lh_attention_fwd_indexed": (i32, [PR, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]),
+        "lh_attention_bwd_indexed": (i32, [PR, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(lib, name)
@@ -226,6 +232,32 @@ def lh_attention_bwd(pr, idx, slot, qs, ks, vs, os_, lse, dout, dq, dk, dv, ws, 
           _stream(stream))
 
 
+def lh_sdpa_fwd_indexed(pr, q, k, v, qpyr, kpyr, vpyr, idx, os_, lse, stream=None):
+    _call("lh_sdpa_fwd_indexed", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(qpyr), _p(kpyr), _p(vpyr), _p(idx),
+          _p(os_), _p(lse), _stream(stream))
+
+
+def lh_sdpa_bwd_indexed(pr, q, k, v, qpyr, kpyr, vpyr, idx, os_, lse, dos, dqs, dks, dvs, ws, ws_bytes=None,
+                        stream=None):
+    _call("lh_sdpa_bwd_indexed", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(qpyr), _p(kpyr), _p(vpyr), _p(idx),
+          _p(os_), _p(lse), _p(dos), _p(dqs), _p(dks), _p(dvs), _p(ws),
+          _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream))
+
+
+def lh_attention_fwd_indexed(pr, q, k, v, o, idx, slot, qpyr, kpyr, vpyr, os_, lse, ws, ws_bytes=None,
+                             stream=None):
+    _call("lh_attention_fwd_indexed", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(o), _p(idx), _p(slot),
+          _p(qpyr), _p(kpyr), _p(vpyr), _p(os_), _p(lse), _p(ws), _nbytes(ws) if ws_bytes is None else ws_bytes,
+          _stream(stream))
+
+
+def lh_attention_bwd_indexed(pr, q, k, v, qpyr, kpyr, vpyr, idx, slot, os_, lse, dout, dq, dk, dv, ws,
+                             ws_bytes=None, stream=None):
+    _call("lh_attention_bwd_indexed", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(qpyr), _p(kpyr), _p(vpyr),
+          _p(idx), _p(slot), _p(os_), _p(lse), _p(dout), _p(dq), _p(dk), _p(dv), _p(ws),
+          _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream))
+
+
 # ---------------------------------------------------------------- allocation helpers
 
 def workspace(pr, op, device="cuda"):
@@ -260,6 +292,47 @@ def attention_forward(q, k, v, p, L, k_budget, scale=0.0, flags=0, stream=None):
                      out["lse"], ws, stream=stream)
     out["ws"] = ws
     return pr, out
+
+
+def attention_forward_indexed(q, k, v, p, L, k_budget, scale=0.0, flags=0, stream=None):
+    """As attention_forward, through lh_attention_fwd_indexed: the state keeps the pyramid
+    (qpyr, kpyr, vpyr) instead of the gathered rows."""
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    pr = problem(B, N, Hq, Hkv, D, p, L, k_budget, q.dtype, scale, flags)
+    st = lh_check(pr)
+    if st != LH_OK:
+        raise LighthouseError(f"lh_check: {lh_status_str(st)}: {lh_last_error()}")
+    S, Ptot = lh_subseq_len(pr), lh_pyramid_rows(pr)
+    R = max(Ptot - N, 1)
+    dev = q.device
+    out = dict(
+        o=torch.empty_like(q),
+        idx=torch.empty(B, Hq, S, dtype=torch.int32, device=dev),
+        slot=torch.empty(B, Hq, Ptot, dtype=torch.int32, device=dev),
+        qpyr=torch.empty(B, R, Hq, D, dtype=q.dtype, device=dev),
+        kpyr=torch.empty(B, R, Hkv, D, dtype=q.dtype, device=dev),
+        vpyr=torch.empty(B, R, Hkv, D, dtype=q.dtype, device=dev),
+        os=torch.empty(B, Hq, S, D, dtype=q.dtype, device=dev),
+        lse=torch.empty(B, Hq, S, dtype=torch.float32, device=dev),
+    )
+    ws = workspace(pr, LH_OP_ATTENTION_FWD_INDEXED, dev)
+    lh_attention_fwd_indexed(pr, q, k, v, out["o"], out["idx"], out["slot"], out["qpyr"], out["kpyr"],
+                             out["vpyr"], out["os"], out["lse"], ws, stream=stream)
+    out["ws"] = ws
+    return pr, out
+
+
+def attention_backward_indexed(pr, q, k, v, state, dout, stream=None):
+    """Allocates dq, dk, dv and runs lh_attention_bwd_indexed from attention_forward_indexed."""
+    B, N, Hq, D = dout.shape
+    dq = torch.empty_like(dout)
+    dk = torch.empty(B, N, pr.Hkv, D, dtype=dout.dtype, device=dout.device)
+    dv = torch.empty_like(dk)
+    ws = workspace(pr, LH_OP_ATTENTION_BWD, dout.device)
+    lh_attention_bwd_indexed(pr, q, k, v, state["qpyr"], state["kpyr"], state["vpyr"], state["idx"],
+                             state["slot"], state["os"], state["lse"], dout, dq, dk, dv, ws, stream=stream)
+    return dq, dk, dv
 
 
 def attention_backward(pr, state, dout, stream=None):

@@ -127,6 +127,7 @@ size_t ws_bytes(const LhShape& s, int op) {
     case LH_OP_SDPA_BWD: return align256((size_t)s.B * s.Hq * s.S * 4);
     case LH_OP_ATTENTION_FWD: return fwd_ws(s).total;
     case LH_OP_ATTENTION_BWD: return bwd_ws(s).total;
+    case LH_OP_ATTENTION_FWD_INDEXED: return fwd_ws(s).total - fwd_ws(s).s_qk;
     default: return (size_t)-1;
   }
 }
@@ -160,6 +161,23 @@ lh_status hip_status(hipError_t e, const char* what) {
 template <typename T>
 T* at(void* base, size_t off) {
   return reinterpret_cast<T*>(reinterpret_cast<unsigned char*>(base) + off);
+}
+
+lh_status need_bf16(const LhShape& s, const char* what) {
+  if (s.dtype != LH_BF16) return fail(LH_E_DTYPE, "%s: the index-driven SDPA is built for bf16 only", what);
+  return LH_OK;
+}
+lh_status need_inputs(const LhShape& s, const void* q, const void* k, const void* v, const void* qp,
+                      const void* kp, const void* vp) {
+  LH_TRY(need_ptr(q, "q"));
+  LH_TRY(need_ptr(k, "k"));
+  LH_TRY(need_ptr(v, "v"));
+  if (s.L > 1) {
+    LH_TRY(need_ptr(qp, "qpyr"));
+    LH_TRY(need_ptr(kp, "kpyr"));
+    LH_TRY(need_ptr(vp, "vpyr"));
+  }
+  return LH_OK;
 }
 
 }  // namespace
@@ -433,6 +451,108 @@ lh_status lh_attention_bwd(const lh_problem* pr, const int32_t* idx, const int32
   LH_TRY(hip_status(lh_launch_scatter_bwd(s, dout, slot, dos, st), "scatter_bwd"));
   LH_TRY(hip_status(lh_launch_sdpa_bwd(s, qs, ks, vs, os, lse, dos, dqs, dks, dvs, at<float>(ws, w.delta), st),
                     "sdpa_bwd"));
+  return hip_status(lh_launch_gather_bwd(s, dqs, dks, dvs, slot, dq, dk, dv, st), "gather_bwd");
+}
+
+
+lh_status lh_sdpa_fwd_indexed(const lh_problem* pr, const void* q, const void* k, const void* v,
+                              const void* qpyr, const void* kpyr, const void* vpyr,
+                              const int32_t* idx, void* os, float* lse, void* stream) {
+  LhShape s;
+  LH_TRY(make_shape(pr, &s));
+  LH_TRY(need_bf16(s, "lh_sdpa_fwd_indexed"));
+  LH_TRY(need_inputs(s, q, k, v, qpyr, kpyr, vpyr));
+  LH_TRY(need_ptr(idx, "idx"));
+  LH_TRY(need_ptr(os, "os"));
+  LH_TRY(need_ptr(lse, "lse"));
+  g_err[0] = 0;
+  return hip_status(lh_launch_sdpa_fwd_indexed(s, q, k, v, qpyr, kpyr, vpyr, idx, os, lse, (hipStream_t)stream),
+                    "lh_sdpa_fwd_indexed");
+}
+
+lh_status lh_sdpa_bwd_indexed(const lh_problem* pr, const void* q, const void* k, const void* v,
+                              const void* qpyr, const void* kpyr, const void* vpyr,
+                              const int32_t* idx, const void* os, const float* lse,
+                              const void* dos, void* dqs, void* dks, void* dvs, void* ws,
+                              size_t ws_bytes_, void* stream) {
+  LhShape s;
+  LH_TRY(make_shape(pr, &s));
+  LH_TRY(need_bf16(s, "lh_sdpa_bwd_indexed"));
+  LH_TRY(need_inputs(s, q, k, v, qpyr, kpyr, vpyr));
+  LH_TRY(need_ptr(idx, "idx"));
+  LH_TRY(need_ptr(os, "os"));
+  LH_TRY(need_ptr(lse, "lse"));
+  LH_TRY(need_ptr(dos, "dos"));
+  LH_TRY(need_ptr(dqs, "dqs"));
+  LH_TRY(need_ptr(dks, "dks"));
+  LH_TRY(need_ptr(dvs, "dvs"));
+  LH_TRY(need_ws(s, LH_OP_SDPA_BWD, ws, ws_bytes_));
+  g_err[0] = 0;
+  return hip_status(lh_launch_sdpa_bwd_indexed(s, q, k, v, qpyr, kpyr, vpyr, idx, os, lse, dos, dqs, dks, dvs,
+                                               (float*)ws, (hipStream_t)stream),
+                    "lh_sdpa_bwd_indexed");
+}
+
+lh_status lh_attention_fwd_indexed(const lh_problem* pr, const void* q, const void* k, const void* v, void* o,
+                                   int32_t* idx, int32_t* slot, void* qpyr, void* kpyr, void* vpyr, void* os,
+                                   float* lse, void* ws, size_t ws_bytes_, void* stream) {
+  LhShape s;
+  LH_TRY(make_shape(pr, &s));
+  LH_TRY(need_bf16(s, "lh_attention_fwd_indexed"));
+  LH_TRY(need_inputs(s, q, k, v, qpyr, kpyr, vpyr));
+  LH_TRY(need_ptr(o, "o"));
+  LH_TRY(need_ptr(idx, "idx"));
+  LH_TRY(need_ptr(slot, "slot"));
+  LH_TRY(need_ptr(os, "os"));
+  LH_TRY(need_ptr(lse, "lse"));
+  LH_TRY(need_ws(s, LH_OP_ATTENTION_FWD_INDEXED, ws, ws_bytes_));
+  g_err[0] = 0;
+  // the workspace holds the scores and selection lists of lh_attention_fwd's, from offset 0
+  const FwdWs w = fwd_ws(s);
+  const size_t base = w.s_qk;
+  hipStream_t st = (hipStream_t)stream;
+  void* qp = s.L > 1 ? qpyr : nullptr;
+  void* kp = s.L > 1 ? kpyr : nullptr;
+  void* vp = s.L > 1 ? vpyr : nullptr;
+  float* sqk = at<float>(ws, w.s_qk - base);
+  float* skq = at<float>(ws, w.s_kq - base);
+  LH_TRY(hip_status(lh_launch_pool_score(s, q, k, v, qp, kp, vp, sqk, skq, st), "pool_score"));
+  LH_TRY(hip_status(lh_launch_select(s, sqk, skq, idx, slot, at<int32_t>(ws, w.sel - base), st), "select"));
+  LH_TRY(hip_status(lh_launch_sdpa_fwd_indexed(s, q, k, v, qp, kp, vp, idx, os, lse, st), "sdpa_fwd_indexed"));
+  return hip_status(lh_launch_scatter(s, os, slot, o, st), "scatter");
+}
+
+lh_status lh_attention_bwd_indexed(const lh_problem* pr, const void* q, const void* k, const void* v,
+                                   const void* qpyr, const void* kpyr, const void* vpyr, const int32_t* idx,
+                                   const int32_t* slot, const void* os, const float* lse, const void* dout,
+                                   void* dq, void* dk, void* dv, void* ws, size_t ws_bytes_, void* stream) {
+  LhShape s;
+  LH_TRY(make_shape(pr, &s));
+  LH_TRY(need_bf16(s, "lh_attention_bwd_indexed"));
+  LH_TRY(need_inputs(s, q, k, v, qpyr, kpyr, vpyr));
+  LH_TRY(need_ptr(idx, "idx"));
+  LH_TRY(need_ptr(slot, "slot"));
+  LH_TRY(need_ptr(os, "os"));
+  LH_TRY(need_ptr(lse, "lse"));
+  LH_TRY(need_ptr(dout, "dout"));
+  LH_TRY(need_ptr(dq, "dq"));
+  LH_TRY(need_ptr(dk, "dk"));
+  LH_TRY(need_ptr(dv, "dv"));
+  LH_TRY(need_ws(s, LH_OP_ATTENTION_BWD, ws, ws_bytes_));
+  g_err[0] = 0;
+  const BwdWs w = bwd_ws(s);
+  hipStream_t st = (hipStream_t)stream;
+  void* dos = at<void>(ws, w.dos);
+  void* dqs = at<void>(ws, w.dqs);
+  void* dks = at<void>(ws, w.dks);
+  void* dvs = at<void>(ws, w.dvs);
+  const void* qp = s.L > 1 ? qpyr : nullptr;
+  const void* kp = s.L > 1 ? kpyr : nullptr;
+  const void* vp = s.L > 1 ? vpyr : nullptr;
+  LH_TRY(hip_status(lh_launch_scatter_bwd(s, dout, slot, dos, st), "scatter_bwd"));
+  LH_TRY(hip_status(lh_launch_sdpa_bwd_indexed(s, q, k, v, qp, kp, vp, idx, os, lse, dos, dqs, dks, dvs,
+                                               at<float>(ws, w.delta), st),
+                    "sdpa_bwd_indexed"));
   return hip_status(lh_launch_gather_bwd(s, dqs, dks, dvs, slot, dq, dk, dv, st), "gather_bwd");
 }
 

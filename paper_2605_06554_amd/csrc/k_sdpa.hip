@@ -9,6 +9,13 @@ hipError_t lh_launch_sdpa_fwd_bf16(const LhShape& s, const void* qs, const void*
 hipError_t lh_launch_sdpa_bwd_bf16(const LhShape& s, const void* qs, const void* ks, const void* vs,
                                    const void* dos, const float* lse, const float* delta, void* dqs,
                                    void* dks, void* dvs, hipStream_t st);
+hipError_t lh_launch_sdpa_fwd_idx(const LhShape& s, const void* q, const void* k, const void* v, const void* qp,
+                                  const void* kp, const void* vp, const int32_t* idx, void* os, float* lse,
+                                  hipStream_t st);
+hipError_t lh_launch_sdpa_bwd_idx(const LhShape& s, const void* q, const void* k, const void* v, const void* qp,
+                                  const void* kp, const void* vp, const int32_t* idx, const void* dos,
+                                  const float* lse, const float* delta, void* dqs, void* dks, void* dvs,
+                                  hipStream_t st);
 
 namespace lh {
 
@@ -201,20 +208,42 @@ hipError_t lh_launch_sdpa_fwd(const LhShape& s, const void* qs, const void* ks, 
   return hipGetLastError();
 }
 
+static hipError_t launch_delta(const LhShape& s, const void* os, const void* dos, float* delta, hipStream_t st) {
+  const int64_t rows = s.B * s.Hq * s.S;
+  const int CPR = s.D / (s.dtype == LH_BF16 ? 8 : 4);
+  dim3 grid((unsigned)((rows * CPR + 255) / 256));
+  if (s.dtype == LH_BF16)
+    hipLaunchKernelGGL(sdpa_delta<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)os, (const bf16_t*)dos, delta, rows, s.D);
+  else
+    hipLaunchKernelGGL(sdpa_delta<float>, grid, dim3(256), 0, st, (const float*)os, (const float*)dos, delta, rows, s.D);
+  return hipGetLastError();
+}
+
+hipError_t lh_launch_sdpa_fwd_indexed(const LhShape& s, const void* q, const void* k, const void* v,
+                                      const void* qpyr, const void* kpyr, const void* vpyr,
+                                      const int32_t* idx, void* os, float* lse, hipStream_t st) {
+  if (s.S == 0) return hipSuccess;
+  return lh_launch_sdpa_fwd_idx(s, q, k, v, qpyr, kpyr, vpyr, idx, os, lse, st);
+}
+
+hipError_t lh_launch_sdpa_bwd_indexed(const LhShape& s, const void* q, const void* k, const void* v,
+                                      const void* qpyr, const void* kpyr, const void* vpyr,
+                                      const int32_t* idx, const void* os, const float* lse,
+                                      const void* dos, void* dqs, void* dks, void* dvs, float* delta,
+                                      hipStream_t st) {
+  if (s.S == 0) return hipSuccess;
+  hipError_t e = launch_delta(s, os, dos, delta, st);
+  if (e != hipSuccess) return e;
+  return lh_launch_sdpa_bwd_idx(s, q, k, v, qpyr, kpyr, vpyr, idx, dos, lse, delta, dqs, dks, dvs, st);
+}
+
 hipError_t lh_launch_sdpa_bwd(const LhShape& s, const void* qs, const void* ks, const void* vs,
                               const void* os, const float* lse, const void* dos, void* dqs,
                               void* dks, void* dvs, float* delta, hipStream_t st) {
   const int64_t BH = s.B * s.Hq;
   if (s.S == 0) return hipSuccess;
-  const int64_t rows = BH * s.S;
-  const int CPR = s.D / (s.dtype == LH_BF16 ? 8 : 4);
   {
-    dim3 grid((unsigned)((rows * CPR + 255) / 256));
-    if (s.dtype == LH_BF16)
-      hipLaunchKernelGGL(sdpa_delta<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)os, (const bf16_t*)dos, delta, rows, s.D);
-    else
-      hipLaunchKernelGGL(sdpa_delta<float>, grid, dim3(256), 0, st, (const float*)os, (const float*)dos, delta, rows, s.D);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_delta(s, os, dos, delta, st);
     if (e != hipSuccess) return e;
   }
   if (s.dtype == LH_BF16) return lh_launch_sdpa_bwd_bf16(s, qs, ks, vs, dos, lse, delta, dqs, dks, dvs, st);

@@ -204,6 +204,70 @@ __device__ __forceinline__ void load_tile(bf16_t* tile, const bf16_t* src, int r
   else load_tile_rows<D, TR, NW, SW, true>(tile, src, r0, S, w, lane);
 }
 
+// Index-driven rows (the gather fused into the loads). Row m of a gathered head is pyramid id
+// idx[m]: ids below N are rows of the input [B, N, H, D], the rest rows of the pyramid
+// [B, R, H, D]. Ids outside [0, N + R) are clamped into it (never an out-of-range read).
+struct SdpaIdx {
+  const bf16_t *q, *k, *v, *qp, *kp, *vp;
+  const int32_t* idx;  // [B, Hq, S]
+  int64_t N, R;
+  int32_t Hq, Hkv, G;
+};
+
+struct RowSrc {
+  const bf16_t* l0;  // row 0 of the head in the input
+  const bf16_t* py;  // row 0 of the head in the pyramid
+  int64_t st;        // elements between consecutive rows: H * D
+  int32_t N, last;   // last = N + R - 1
+};
+
+__device__ __forceinline__ RowSrc row_src(const bf16_t* x, const bf16_t* pyr, int64_t b, int h, int H,
+                                          const SdpaIdx& ix, int D) {
+  RowSrc r;
+  r.st = (int64_t)H * D;
+  r.l0 = x + (b * ix.N * H + h) * D;
+  r.py = pyr + (b * ix.R * H + h) * D;
+  r.N = (int32_t)ix.N;
+  r.last = (int32_t)(ix.N + ix.R - 1);
+  return r;
+}
+
+__device__ __forceinline__ const bf16_t* rs_row(const RowSrc& s, int32_t id) {
+  id = id < 0 ? 0 : id > s.last ? s.last : id;
+  return id < s.N ? s.l0 + (int64_t)id * s.st : s.py + (int64_t)(id - s.N) * s.st;
+}
+
+// Pyramid ids of the rows this lane copies in load_tile (rows past S take row S - 1's id).
+template <int D, int TR, int NW>
+__device__ __forceinline__ void tile_ids(const int32_t* idxh, int r0, int S, int w, int lane, int32_t* ids) {
+  constexpr int CPR = D / 8;
+  constexpr int BLOCKS = TR * CPR / 64;
+#pragma unroll
+  for (int j = 0; j < loads_per_wave<D, TR, NW>(); ++j) {
+    int blk = j * NW + w;
+    if (BLOCKS % NW != 0 && blk >= BLOCKS) blk -= BLOCKS;
+    const int gr = r0 + (blk * 64 + lane) / CPR;
+    ids[j] = idxh[gr < S ? gr : S - 1];
+  }
+}
+
+// load_tile with every row read from its pyramid id.
+template <int D, int TR, int NW, int SW>
+__device__ __forceinline__ void load_tile_idx(bf16_t* tile, const RowSrc& src, const int32_t* ids, int w, int lane) {
+  constexpr int CPR = D / 8;
+  constexpr int BLOCKS = TR * CPR / 64;
+#pragma unroll
+  for (int j = 0; j < loads_per_wave<D, TR, NW>(); ++j) {
+    int blk = j * NW + w;
+    if (BLOCKS % NW != 0 && blk >= BLOCKS) blk -= BLOCKS;
+    const int pos = blk * 64 + lane;
+    const int c = (pos % CPR) ^ swz<D, SW>(pos / CPR);
+    const bf16_t* g = rs_row(src, ids[j]) + c * 8;
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
+                                     (__attribute__((address_space(3))) void*)(tile + blk * 512), 16, 0, 0);
+  }
+}
+
 // Waits until at most N of this wave's vector-memory loads are outstanding and every LDS
 // access of the wave has completed (s_waitcnt vmcnt(N) lgkmcnt(0)), then joins the block
 // barrier. The empty asm statements keep the compiler from moving memory accesses across.
@@ -272,10 +336,11 @@ __device__ __forceinline__ void store_qrow(bf16_t* row, const f32x16* acc, float
 // ------------------------------------------------------------------ forward
 constexpr int FW = LH_FW, FQ = 32 * LH_FW, FK = LH_FK, FNS = LH_FNS;
 
-template <int D>
+// IDX: Q, K, V are unused; rows come from the input / pyramid through ix.idx.
+template <int D, bool IDX>
 __global__ void __launch_bounds__(64 * FW) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
-              bf16_t* __restrict__ O, float* __restrict__ LSE, int S, float sl2) {
+              bf16_t* __restrict__ O, float* __restrict__ LSE, int S, float sl2, SdpaIdx ix) {
   constexpr int RB = 2 * D;
   constexpr int NB = FK / 32;  // 32-key blocks per tile
   constexpr int LPT = 2 * loads_per_wave<D, FK, FW>();
@@ -293,18 +358,43 @@ sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const 
   const bf16_t* Kh = K + bh * S * D;
   const bf16_t* Vh = V + bh * S * D;
   const LaneOff<D> lo = lane_offsets<D, LH_SWZ_F>(lane);
+  constexpr int LPW = loads_per_wave<D, FK, FW>();
+  RowSrc qsrc{}, ksrc{}, vsrc{};
+  const int32_t* idxh = nullptr;
+  int32_t kv_ids[LPW];  // ids of the next tile to be loaded
+  if constexpr (IDX) {
+    const int64_t b = bh / ix.Hq;
+    const int hq = (int)(bh - b * ix.Hq), g = hq / ix.G;
+    qsrc = row_src(ix.q, ix.qp, b, hq, ix.Hq, ix, D);
+    ksrc = row_src(ix.k, ix.kp, b, g, ix.Hkv, ix, D);
+    vsrc = row_src(ix.v, ix.vp, b, g, ix.Hkv, ix, D);
+    idxh = ix.idx + bh * S;
+  }
+  auto load_kv = [&](int slot_, int r0) __attribute__((always_inline)) {
+    bf16_t* kt_ = slot_ == 0 ? Ks[0] : slot_ == 1 ? Ks[1] : slot_ == 2 ? Ks[2] : Ks[3];
+    bf16_t* vt_ = slot_ == 0 ? Vs[0] : slot_ == 1 ? Vs[1] : slot_ == 2 ? Vs[2] : Vs[3];
+    if constexpr (IDX) {
+      load_tile_idx<D, FK, FW, LH_SWZ_F>(kt_, ksrc, kv_ids, w, lane);
+      load_tile_idx<D, FK, FW, LH_SWZ_F>(vt_, vsrc, kv_ids, w, lane);
+      tile_ids<D, FK, FW>(idxh, r0 + FK, S, w, lane, kv_ids);  // the tile after this one
+    } else {
+      load_tile<D, FK, FW, LH_SWZ_F>(kt_, Kh, r0, S, w, lane);
+      load_tile<D, FK, FW, LH_SWZ_F>(vt_, Vh, r0, S, w, lane);
+    }
+  };
+  if constexpr (IDX) tile_ids<D, FK, FW>(idxh, 0, S, w, lane, kv_ids);
 
   const int kend = q0 + FQ < S ? q0 + FQ : S;
   const int nkt = (kend + FK - 1) / FK;
   bf16x8 qreg[D / 16];
   const int qrow = myq < S ? myq : S - 1;
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) qreg[kk] = gld8(Qh + (int64_t)qrow * D + 16 * kk + 8 * h);
-#pragma unroll
-  for (int t = 0; t < FNS - 1; ++t) {
-    load_tile<D, FK, FW, LH_SWZ_F>(Ks[t], Kh, t * FK, S, w, lane);
-    load_tile<D, FK, FW, LH_SWZ_F>(Vs[t], Vh, t * FK, S, w, lane);
+  for (int kk = 0; kk < D / 16; ++kk) {
+    const bf16_t* qr = IDX ? rs_row(qsrc, idxh[qrow]) : Qh + (int64_t)qrow * D;
+    qreg[kk] = gld8(qr + 16 * kk + 8 * h);
   }
+#pragma unroll
+  for (int t = 0; t < FNS - 1; ++t) load_kv(t, t * FK);
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int d = 0; d < D / 32; ++d) oacc[d] = f32x16{};
@@ -314,8 +404,7 @@ sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const 
     constexpr int SL = decltype(slotc)::value;
     constexpr int NX = (SL + FNS - 1) % FNS;  // slot of tile kt + FNS - 1 (tile kt - 1's)
     sync_tiles<(FNS - 2) * LPT>();  // tile kt landed in every wave; tile kt - 1 is done
-    load_tile<D, FK, FW, LH_SWZ_F>(Ks[NX], Kh, (kt + FNS - 1) * FK, S, w, lane);
-    load_tile<D, FK, FW, LH_SWZ_F>(Vs[NX], Vh, (kt + FNS - 1) * FK, S, w, lane);
+    load_kv(NX, (kt + FNS - 1) * FK);
     const int k0 = kt * FK;
     if (qw + 31 < k0) return;  // every key of the tile is in the future of this wave's rows
     const bf16_t* Kt = Ks[SL];
@@ -377,11 +466,11 @@ sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const 
 // P = exp2(S scale log2e - lse log2e) and dS = P (dP - Delta); dQ^T += K^T dS^T.
 constexpr int QW = LH_QW, BQ = 32 * LH_QW, BK = LH_BK, QNS = LH_QNS;
 
-template <int D>
+template <int D, bool IDX>
 __global__ void __launch_bounds__(64 * QW) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
                  const bf16_t* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ DELTA,
-                 bf16_t* __restrict__ dQ, int S, float sl2, float scale) {
+                 bf16_t* __restrict__ dQ, int S, float sl2, float scale, SdpaIdx ix) {
   constexpr int RB = 2 * D;
   constexpr int LPT = 2 * loads_per_wave<D, BK, QW>();
   static_assert(QNS >= 2 && QNS <= 4, "ring of 2 to 4 slots");
@@ -399,6 +488,31 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
   const bf16_t* Vh = V + bh * S * D;
   const bf16_t* dOh = dO + bh * S * D;
   const LaneOff<D> lo = lane_offsets<D, LH_SWZ_Q>(lane);
+  constexpr int LPW = loads_per_wave<D, BK, QW>();
+  RowSrc qsrc{}, ksrc{}, vsrc{};
+  const int32_t* idxh = nullptr;
+  int32_t kv_ids[LPW];  // ids of the next tile to be loaded
+  if constexpr (IDX) {
+    const int64_t b = bh / ix.Hq;
+    const int hq = (int)(bh - b * ix.Hq), g = hq / ix.G;
+    qsrc = row_src(ix.q, ix.qp, b, hq, ix.Hq, ix, D);
+    ksrc = row_src(ix.k, ix.kp, b, g, ix.Hkv, ix, D);
+    vsrc = row_src(ix.v, ix.vp, b, g, ix.Hkv, ix, D);
+    idxh = ix.idx + bh * S;
+    tile_ids<D, BK, QW>(idxh, 0, S, w, lane, kv_ids);
+  }
+  auto load_kv = [&](int slot_, int r0) __attribute__((always_inline)) {
+    bf16_t* kt_ = slot_ == 0 ? Ks[0] : slot_ == 1 ? Ks[1] : slot_ == 2 ? Ks[2] : Ks[3];
+    bf16_t* vt_ = slot_ == 0 ? Vs[0] : slot_ == 1 ? Vs[1] : slot_ == 2 ? Vs[2] : Vs[3];
+    if constexpr (IDX) {
+      load_tile_idx<D, BK, QW, LH_SWZ_Q>(kt_, ksrc, kv_ids, w, lane);
+      load_tile_idx<D, BK, QW, LH_SWZ_Q>(vt_, vsrc, kv_ids, w, lane);
+      tile_ids<D, BK, QW>(idxh, r0 + BK, S, w, lane, kv_ids);
+    } else {
+      load_tile<D, BK, QW, LH_SWZ_Q>(kt_, Kh, r0, S, w, lane);
+      load_tile<D, BK, QW, LH_SWZ_Q>(vt_, Vh, r0, S, w, lane);
+    }
+  };
 
   const int kend = q0 + BQ < S ? q0 + BQ : S;
   const int nkt = (kend + BK - 1) / BK;
@@ -406,16 +520,14 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
   bf16x8 qreg[D / 16], doreg[D / 16];
 #pragma unroll
   for (int kk = 0; kk < D / 16; ++kk) {
-    qreg[kk] = gld8(Qh + (int64_t)qrow * D + 16 * kk + 8 * h);
+    const bf16_t* qr = IDX ? rs_row(qsrc, idxh[qrow]) : Qh + (int64_t)qrow * D;
+    qreg[kk] = gld8(qr + 16 * kk + 8 * h);
     doreg[kk] = gld8(dOh + (int64_t)qrow * D + 16 * kk + 8 * h);
   }
   const float lse2 = myq < S ? LSE[bh * S + myq] * kLog2e : INFINITY;
   const float dlt = myq < S ? DELTA[bh * S + myq] : 0.0f;
 #pragma unroll
-  for (int t = 0; t < QNS - 1; ++t) {
-    load_tile<D, BK, QW, LH_SWZ_Q>(Ks[t], Kh, t * BK, S, w, lane);
-    load_tile<D, BK, QW, LH_SWZ_Q>(Vs[t], Vh, t * BK, S, w, lane);
-  }
+  for (int t = 0; t < QNS - 1; ++t) load_kv(t, t * BK);
   f32x16 dqacc[D / 32];
 #pragma unroll
   for (int d = 0; d < D / 32; ++d) dqacc[d] = f32x16{};
@@ -428,8 +540,7 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
     constexpr bool MASK = decltype(maskc)::value != 0;
     constexpr int NX = (SL + QNS - 1) % QNS;
     sync_tiles<(QNS - 2) * LPT>();
-    load_tile<D, BK, QW, LH_SWZ_Q>(Ks[NX], Kh, (kt + QNS - 1) * BK, S, w, lane);
-    load_tile<D, BK, QW, LH_SWZ_Q>(Vs[NX], Vh, (kt + QNS - 1) * BK, S, w, lane);
+    load_kv(NX, (kt + QNS - 1) * BK);
     const int k0 = kt * BK;
     if (qw + 31 < k0) return;
     const bf16_t* Kt = Ks[SL];
@@ -478,11 +589,11 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
 constexpr int KWV = LH_KWV, CK = 32 * LH_KWV, CQ = LH_CQ;
 static_assert(CQ % 32 == 0 && CQ <= 64, "query tile of 32 or 64 rows");
 
-template <int D>
+template <int D, bool IDX>
 __global__ void __launch_bounds__(64 * KWV) __attribute__((amdgpu_waves_per_eu(LH_KWV_EU, LH_KWV_EU)))
 sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
                    const bf16_t* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ DELTA,
-                   bf16_t* __restrict__ dK, bf16_t* __restrict__ dV, int S, float sl2, float scale) {
+                   bf16_t* __restrict__ dK, bf16_t* __restrict__ dV, int S, float sl2, float scale, SdpaIdx ix) {
   constexpr int RB = 2 * D;
   // LDS is laid out by decreasing alignment: the lse / Delta rows (1 KB) first, then the query
   // tiles, so that both sit inside the first 64 KB, where a base address folds into the 16-bit
@@ -503,30 +614,52 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
   const float* Lh = LSE + bh * S;
   const float* Dh = DELTA + bh * S;
   const LaneOff<D> lo = lane_offsets<D, LH_SWZ_K>(lane);
+  RowSrc qsrc{}, ksrc{}, vsrc{};
+  const int32_t* idxh = nullptr;
+  int32_t q_ids[loads_per_wave<D, CQ, KWV>()];  // ids of the next query tile to be staged
+  if constexpr (IDX) {
+    const int64_t b = bh / ix.Hq;
+    const int hq = (int)(bh - b * ix.Hq), g = hq / ix.G;
+    qsrc = row_src(ix.q, ix.qp, b, hq, ix.Hq, ix, D);
+    ksrc = row_src(ix.k, ix.kp, b, g, ix.Hkv, ix, D);
+    vsrc = row_src(ix.v, ix.vp, b, g, ix.Hkv, ix, D);
+    idxh = ix.idx + bh * S;
+  }
 
   const int qstart = (k0 / CQ) * CQ;
   const int nqt = (S - qstart + CQ - 1) / CQ;
   auto stage = [&](auto bufc, int qt0) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value;
-    load_tile<D, CQ, KWV, LH_SWZ_K>(BUF ? Qs1 : Qs0, Qh, qt0, S, w, lane);
+    if constexpr (IDX) load_tile_idx<D, CQ, KWV, LH_SWZ_K>(BUF ? Qs1 : Qs0, qsrc, q_ids, w, lane);
+    else load_tile<D, CQ, KWV, LH_SWZ_K>(BUF ? Qs1 : Qs0, Qh, qt0, S, w, lane);
     load_tile<D, CQ, KWV, LH_SWZ_K>(BUF ? dOs1 : dOs0, dOh, qt0, S, w, lane);
     if (tid < CQ) {
       const int q = qt0 + tid;
       (BUF ? ls1 : ls0)[tid] = q < S ? Lh[q] * kLog2e : INFINITY;  // rows past S: P = 0
       (BUF ? ds1 : ds0)[tid] = q < S ? -Dh[q] : 0.0f;  // negated: it seeds the dP accumulator
     }
+    // tiles are staged from the last one down: the next one starts CQ rows earlier
+    if constexpr (IDX) tile_ids<D, CQ, KWV>(idxh, qt0 - CQ > 0 ? qt0 - CQ : 0, S, w, lane, q_ids);
   };
   // Query tiles are visited from the last one down to the diagonal: every key block of a head
   // then starts on the same tile and streams the same tiles in step with the others, so the
   // blocks running together on an XCD share each Q / dO tile through its L2.
   const int qlast = qstart + (nqt - 1) * CQ;
-  load_tile<D, CK, KWV, LH_SWZ_K>(Kw, Kh, k0, S, w, lane);
+  if constexpr (IDX) {
+    int32_t k_ids[loads_per_wave<D, CK, KWV>()];
+    tile_ids<D, CK, KWV>(idxh, k0, S, w, lane, k_ids);
+    load_tile_idx<D, CK, KWV, LH_SWZ_K>(Kw, ksrc, k_ids, w, lane);
+    tile_ids<D, CQ, KWV>(idxh, qlast, S, w, lane, q_ids);
+  } else {
+    load_tile<D, CK, KWV, LH_SWZ_K>(Kw, Kh, k0, S, w, lane);
+  }
   stage(IC<0>{}, qlast);
 
   const int krow = mykey < S ? mykey : S - 1;
+  const bf16_t* vrow = IDX ? rs_row(vsrc, idxh[krow]) : Vh + (int64_t)krow * D;
   bf16x8 vreg[D / 16];
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) vreg[kk] = gld8(Vh + (int64_t)krow * D + 16 * kk + 8 * h);
+  for (int kk = 0; kk < D / 16; ++kk) vreg[kk] = gld8(vrow + 16 * kk + 8 * h);
   f32x16 dkacc[D / 32], dvacc[D / 32];
 #pragma unroll
   for (int d = 0; d < D / 32; ++d) dkacc[d] = dvacc[d] = f32x16{};
@@ -610,26 +743,25 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
     }
 }
 
-}  // namespace lh
-
-using namespace lh;
-
-hipError_t lh_launch_sdpa_fwd_bf16(const LhShape& s, const void* qs, const void* ks, const void* vs, void* os,
-                                   float* lse, hipStream_t st) {
+template <bool IDX>
+static void launch_fwd(const LhShape& s, const void* qs, const void* ks, const void* vs, void* os, float* lse,
+                       const SdpaIdx& ix, hipStream_t st) {
   const int S = (int)s.S;
   dim3 grid((unsigned)((S + FQ - 1) / FQ), (unsigned)(s.B * s.Hq));
   const float sl2 = s.scale * kLog2e;
   auto q = (const bf16_t*)qs;
   auto k = (const bf16_t*)ks;
   auto v = (const bf16_t*)vs;
-  if (s.D == 128) hipLaunchKernelGGL(sdpa_fwd_bf16<128>, grid, dim3(64 * FW), 0, st, q, k, v, (bf16_t*)os, lse, S, sl2);
-  else hipLaunchKernelGGL(sdpa_fwd_bf16<64>, grid, dim3(64 * FW), 0, st, q, k, v, (bf16_t*)os, lse, S, sl2);
-  return hipGetLastError();
+  if (s.D == 128)
+    hipLaunchKernelGGL((sdpa_fwd_bf16<128, IDX>), grid, dim3(64 * FW), 0, st, q, k, v, (bf16_t*)os, lse, S, sl2, ix);
+  else
+    hipLaunchKernelGGL((sdpa_fwd_bf16<64, IDX>), grid, dim3(64 * FW), 0, st, q, k, v, (bf16_t*)os, lse, S, sl2, ix);
 }
 
-hipError_t lh_launch_sdpa_bwd_bf16(const LhShape& s, const void* qs, const void* ks, const void* vs,
-                                   const void* dos, const float* lse, const float* delta, void* dqs,
-                                   void* dks, void* dvs, hipStream_t st) {
+template <bool IDX>
+static void launch_bwd(const LhShape& s, const void* qs, const void* ks, const void* vs, const void* dos,
+                       const float* lse, const float* delta, void* dqs, void* dks, void* dvs, const SdpaIdx& ix,
+                       hipStream_t st) {
   const int S = (int)s.S;
   const int64_t BH = s.B * s.Hq;
   const float sl2 = s.scale * kLog2e;
@@ -640,15 +772,61 @@ hipError_t lh_launch_sdpa_bwd_bf16(const LhShape& s, const void* qs, const void*
   dim3 gk((unsigned)((S + CK - 1) / CK), (unsigned)BH);
   dim3 gq((unsigned)((S + BQ - 1) / BQ), (unsigned)BH);
   if (s.D == 128) {
-    hipLaunchKernelGGL(sdpa_bwd_dkdv_bf16<128>, gk, dim3(64 * KWV), 0, st, q, k, v, g, lse, delta, (bf16_t*)dks,
-                       (bf16_t*)dvs, S, sl2, s.scale);
-    hipLaunchKernelGGL(sdpa_bwd_dq_bf16<128>, gq, dim3(64 * QW), 0, st, q, k, v, g, lse, delta, (bf16_t*)dqs, S, sl2,
-                       s.scale);
+    hipLaunchKernelGGL((sdpa_bwd_dkdv_bf16<128, IDX>), gk, dim3(64 * KWV), 0, st, q, k, v, g, lse, delta,
+                       (bf16_t*)dks, (bf16_t*)dvs, S, sl2, s.scale, ix);
+    hipLaunchKernelGGL((sdpa_bwd_dq_bf16<128, IDX>), gq, dim3(64 * QW), 0, st, q, k, v, g, lse, delta,
+                       (bf16_t*)dqs, S, sl2, s.scale, ix);
   } else {
-    hipLaunchKernelGGL(sdpa_bwd_dkdv_bf16<64>, gk, dim3(64 * KWV), 0, st, q, k, v, g, lse, delta, (bf16_t*)dks,
-                       (bf16_t*)dvs, S, sl2, s.scale);
-    hipLaunchKernelGGL(sdpa_bwd_dq_bf16<64>, gq, dim3(64 * QW), 0, st, q, k, v, g, lse, delta, (bf16_t*)dqs, S, sl2,
-                       s.scale);
+    hipLaunchKernelGGL((sdpa_bwd_dkdv_bf16<64, IDX>), gk, dim3(64 * KWV), 0, st, q, k, v, g, lse, delta,
+                       (bf16_t*)dks, (bf16_t*)dvs, S, sl2, s.scale, ix);
+    hipLaunchKernelGGL((sdpa_bwd_dq_bf16<64, IDX>), gq, dim3(64 * QW), 0, st, q, k, v, g, lse, delta,
+                       (bf16_t*)dqs, S, sl2, s.scale, ix);
   }
+}
+
+static SdpaIdx make_idx(const LhShape& s, const void* q, const void* k, const void* v, const void* qp,
+                        const void* kp, const void* vp, const int32_t* idx) {
+  SdpaIdx ix{};
+  ix.q = (const bf16_t*)q, ix.k = (const bf16_t*)k, ix.v = (const bf16_t*)v;
+  // with L = 1 there is no pyramid: every id is below N, the pointers are never followed
+  ix.qp = qp ? (const bf16_t*)qp : ix.q;
+  ix.kp = kp ? (const bf16_t*)kp : ix.k;
+  ix.vp = vp ? (const bf16_t*)vp : ix.v;
+  ix.idx = idx;
+  ix.N = s.N, ix.R = s.R > 0 ? s.R : 0;
+  ix.Hq = s.Hq, ix.Hkv = s.Hkv, ix.G = s.G;
+  return ix;
+}
+
+}  // namespace lh
+
+using namespace lh;
+
+hipError_t lh_launch_sdpa_fwd_bf16(const LhShape& s, const void* qs, const void* ks, const void* vs, void* os,
+                                   float* lse, hipStream_t st) {
+  launch_fwd<false>(s, qs, ks, vs, os, lse, SdpaIdx{}, st);
+  return hipGetLastError();
+}
+
+hipError_t lh_launch_sdpa_bwd_bf16(const LhShape& s, const void* qs, const void* ks, const void* vs,
+                                   const void* dos, const float* lse, const float* delta, void* dqs,
+                                   void* dks, void* dvs, hipStream_t st) {
+  launch_bwd<false>(s, qs, ks, vs, dos, lse, delta, dqs, dks, dvs, SdpaIdx{}, st);
+  return hipGetLastError();
+}
+
+hipError_t lh_launch_sdpa_fwd_idx(const LhShape& s, const void* q, const void* k, const void* v, const void* qp,
+                                  const void* kp, const void* vp, const int32_t* idx, void* os, float* lse,
+                                  hipStream_t st) {
+  launch_fwd<true>(s, nullptr, nullptr, nullptr, os, lse, make_idx(s, q, k, v, qp, kp, vp, idx), st);
+  return hipGetLastError();
+}
+
+hipError_t lh_launch_sdpa_bwd_idx(const LhShape& s, const void* q, const void* k, const void* v, const void* qp,
+                                  const void* kp, const void* vp, const int32_t* idx, const void* dos,
+                                  const float* lse, const float* delta, void* dqs, void* dks, void* dvs,
+                                  hipStream_t st) {
+  launch_bwd<true>(s, nullptr, nullptr, nullptr, dos, lse, delta, dqs, dks, dvs,
+                   make_idx(s, q, k, v, qp, kp, vp, idx), st);
   return hipGetLastError();
 }

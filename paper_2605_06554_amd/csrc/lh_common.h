@@ -142,3 +142,12 @@ hipError_t lh_launch_sdpa_fwd(const LhShape& s, const void* qs, const void* ks, 
 hipError_t lh_launch_sdpa_bwd(const LhShape& s, const void* qs, const void* ks, const void* vs,
                               const void* os, const float* lse, const void* dos, void* dqs,
                               void* dks, void* dvs, float* delta, hipStream_t st);
+// Index-driven SDPA (bf16): rows of Q~, K~, V~ are read from the inputs and pyramids through idx.
+hipError_t lh_launch_sdpa_fwd_indexed(const LhShape& s, const void* q, const void* k, const void* v,
+                                      const void* qpyr, const void* kpyr, const void* vpyr,
+                                      const int32_t* idx, void* os, float* lse, hipStream_t st);
+hipError_t lh_launch_sdpa_bwd_indexed(const LhShape& s, const void* q, const void* k, const void* v,
+                                      const void* qpyr, const void* kpyr, const void* vpyr,
+                                      const int32_t* idx, const void* os, const float* lse,
+                                      const void* dos, void* dqs, void* dks, void* dvs, float* delta,
+                                      hipStream_t st);

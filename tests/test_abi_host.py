@@ -117,3 +117,30 @@ def test_entry_points_reject_bad_pointers_before_any_launch():
     assert lib.lh_select_topk(ctypes.byref(pr), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 16, None) == -6
     bad = _pr(N=1000)
     assert lib.lh_sdpa_fwd(ctypes.byref(bad), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, None) == -2
+
+
+def test_indexed_entry_points_are_bf16_only():
+    """The index-driven SDPA is built for bf16: fp32 problems are rejected on the host, before
+    any pointer is looked at or anything is launched."""
+    pr = _pr(dtype=lh.LH_F32)
+    lib = lh._load()
+    z = None
+    assert lib.lh_sdpa_fwd_indexed(ctypes.byref(pr), z, z, z, z, z, z, z, z, z, z) == -4
+    assert "bf16" in lh.lh_last_error()
+    assert lib.lh_sdpa_bwd_indexed(ctypes.byref(pr), *([z] * 14), 0, z) == -4
+    assert lib.lh_attention_fwd_indexed(ctypes.byref(pr), *([z] * 12), 0, z) == -4
+    assert lib.lh_attention_bwd_indexed(ctypes.byref(pr), *([z] * 15), 0, z) == -4
+    # bf16 with a NULL input is a pointer error, still on the host
+    pr16 = _pr(dtype=lh.LH_BF16)
+    assert lib.lh_sdpa_fwd_indexed(ctypes.byref(pr16), z, z, z, z, z, z, z, z, z, z) == -1
+
+
+def test_indexed_forward_workspace_is_the_scores_and_lists():
+    """lh_attention_fwd_indexed keeps no pyramid in its workspace: it needs the forward
+    workspace minus the three pyramid buffers."""
+    pr = _pr(dtype=lh.LH_BF16, B=2, N=4096, Hq=4, Hkv=2, D=128, p=4, L=4, k=256)
+    full = lh.lh_workspace_bytes(pr, lh.LH_OP_ATTENTION_FWD)
+    idx = lh.lh_workspace_bytes(pr, lh.LH_OP_ATTENTION_FWD_INDEXED)
+    R = lh.lh_pyramid_rows(pr) - 4096
+    al = lambda n: (n + 255) // 256 * 256
+    assert full - idx == al(2 * R * 4 * 128 * 2) + 2 * al(2 * R * 2 * 128 * 2)
