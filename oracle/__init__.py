@@ -26,6 +26,10 @@ F32, BF16, F64 = 0, 1, 2  # F64: unrounded pooled storage (finite-difference pin
 REPLACE_PARENTS = 1
 STRATIFIED = 2
 STRAT_CHUNK = 2048  # chunk of the stratified selection (App. D.2)
+# One selection per KV group (GQA-shared): the group's query score stream is the elementwise max
+# of its query heads' streams, combined with the KV head's stream by the same max as Eq. topk
+# combines s_QK and s_KQ. A layer-level flag: the per-head functions above do not see it.
+GQA_SHARED = 4
 
 
 def build(force: bool = True) -> str:
@@ -259,12 +263,33 @@ def head_forward(h: Head, scale: float, q: np.ndarray, k: np.ndarray, v: np.ndar
     return dict(s_qk=s_qk, s_kq=s_kq, idx=idx, slot=slot, qs=qs, ks=ks, vs=vs, os=os_, lse=lse, o=o)
 
 
+def group_forward(h: Head, scale: float, qg: list, k: np.ndarray, v: np.ndarray):
+    """One (b, KV group) problem with a shared selection. qg: the group's query-head slices
+    [N, D]; k, v: the KV head's slices. The selection ranks by max(max over the group of
+    s_QK, s_KQ); every query head attends over the group's gathered K~, V~."""
+    s_qk_heads = [scores(h, q) for q in qg]
+    s_qk = np.maximum.reduce(s_qk_heads)
+    s_kq = scores(h, k)
+    idx, slot = select(h, s_qk, s_kq)
+    ks = gather(h, pool(h, k), idx)
+    vs = gather(h, pool(h, v), idx)
+    heads = []
+    for q, sq in zip(qg, s_qk_heads):
+        qs = gather(h, pool(h, q), idx)
+        os_, lse = sdpa_fwd(qs, ks, vs, scale)
+        heads.append(dict(s_qk=sq, qs=qs, os=os_, lse=lse, o=scatter(h, idx, os_)))
+    return dict(idx=idx, slot=slot, s_kq=s_kq, ks=ks, vs=vs, heads=heads)
+
+
 def layer_forward(q, k, v, p, L, kk, dtype=BF16, scale=0.0, flags=0):
     """Whole layer for small problems: q [B,N,Hq,D], k/v [B,N,Hkv,D] float64.
-    Returns a dict of per-(b,hq) results stacked as [B, Hq, ...] plus o [B,N,Hq,D]."""
+    Returns a dict of per-(b,hq) results stacked as [B, Hq, ...] plus o [B,N,Hq,D]. With
+    GQA_SHARED in flags, idx, slot, ks and vs are per KV head: [B, Hkv, ...]."""
     B, N, Hq, D = q.shape
     Hkv = k.shape[2]
     G = Hq // Hkv
+    if flags & GQA_SHARED:
+        return _layer_forward_shared(q, k, v, p, L, kk, dtype, scale, flags & ~GQA_SHARED)
     h = Head(N, D, p, L, kk, dtype, flags)
     sc = default_scale(D, scale)
     res = [[head_forward(h, sc, q[b, :, hq, :], k[b, :, hq // G, :], v[b, :, hq // G, :])
@@ -278,8 +303,33 @@ def layer_forward(q, k, v, p, L, kk, dtype=BF16, scale=0.0, flags=0):
     return out
 
 
+def _layer_forward_shared(q, k, v, p, L, kk, dtype, scale, flags):
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    G = Hq // Hkv
+    h = Head(N, D, p, L, kk, dtype, flags)
+    sc = default_scale(D, scale)
+    res = [[group_forward(h, sc, [q[b, :, g * G + t, :] for t in range(G)], k[b, :, g, :], v[b, :, g, :])
+            for g in range(Hkv)] for b in range(B)]
+    out = {key: np.stack([np.stack([res[b][g][key] for g in range(Hkv)]) for b in range(B)])
+           for key in ("idx", "slot", "s_kq", "ks", "vs")}
+    for key in ("s_qk", "qs", "os", "lse"):
+        out[key] = np.stack([np.stack([res[b][hq // G]["heads"][hq % G][key] for hq in range(Hq)])
+                             for b in range(B)])
+    out["o"] = np.stack([np.stack([res[b][hq // G]["heads"][hq % G]["o"] for hq in range(Hq)], axis=1)
+                         for b in range(B)])
+    out["head"] = h
+    out["scale"] = sc
+    out["shared"] = True
+    return out
+
+
 def layer_backward(fwd, dout):
-    """Backward of layer_forward from dout [B,N,Hq,D] float64: (dq, dk, dv, dos, dqs, dks, dvs)."""
+    """Backward of layer_forward from dout [B,N,Hq,D] float64: (dq, dk, dv, dos, dqs, dks, dvs).
+    With a shared selection, dks and dvs are per KV head: the sums over the group's query heads
+    of each head's gradient of the shared K~, V~."""
+    if fwd.get("shared"):
+        return _layer_backward_shared(fwd, dout)
     h = fwd["head"]
     sc = fwd["scale"]
     B, Hq, S = fwd["idx"].shape
@@ -309,4 +359,39 @@ def layer_backward(fwd, dout):
             tv = np.zeros((N, D))
             gather_pool_bwd(h, idx, dvs[b, hq], tv)
             dv[b, :, hq // G, :] += tv
+    return dict(dq=dq, dk=dk, dv=dv, dos=dos, dqs=dqs, dks=dks, dvs=dvs)
+
+
+def _layer_backward_shared(fwd, dout):
+    h = fwd["head"]
+    sc = fwd["scale"]
+    B, Hq, S = fwd["qs"].shape[:3]
+    Hkv = fwd["idx"].shape[1]
+    G = Hq // Hkv
+    N, D = h.N, h.D
+    dq = np.zeros((B, N, Hq, D))
+    dk = np.zeros((B, N, Hkv, D))
+    dv = np.zeros((B, N, Hkv, D))
+    dos = np.zeros((B, Hq, S, D))
+    dqs = np.zeros((B, Hq, S, D))
+    dks = np.zeros((B, Hkv, S, D))
+    dvs = np.zeros((B, Hkv, S, D))
+    for b in range(B):
+        for g in range(Hkv):
+            idx = fwd["idx"][b, g]
+            for hq in range(g * G, (g + 1) * G):
+                dos[b, hq] = scatter_bwd(h, idx, np.ascontiguousarray(dout[b, :, hq, :]))
+                dqs[b, hq], tk, tv = sdpa_bwd(fwd["qs"][b, hq], fwd["ks"][b, g], fwd["vs"][b, g],
+                                              fwd["os"][b, hq], fwd["lse"][b, hq], dos[b, hq], sc)
+                dks[b, g] += tk
+                dvs[b, g] += tv
+                tq = np.zeros((N, D))
+                gather_pool_bwd(h, idx, dqs[b, hq], tq)
+                dq[b, :, hq, :] = tq
+            tk = np.zeros((N, D))
+            gather_pool_bwd(h, idx, dks[b, g], tk)
+            dk[b, :, g, :] = tk
+            tv = np.zeros((N, D))
+            gather_pool_bwd(h, idx, dvs[b, g], tv)
+            dv[b, :, g, :] = tv
     return dict(dq=dq, dk=dk, dv=dv, dos=dos, dqs=dqs, dks=dks, dvs=dvs)

@@ -156,3 +156,39 @@ def select_stratified(sqk_levels, skq_levels, p, L, k, chunk):
                 parents += seen
         cand = sorted(p * i + r for i in parents for r in range(p))
     return emitted
+
+
+def select_group_stream(sqk_levels_heads, skq_levels, p, L, k):
+    """Per-level descent for a selection shared by a KV group: each level's parents are the
+    first k DISTINCT entries of the concatenation of every query head's QK stream and the KV
+    head's KQ stream, walked in (score desc, index asc) order. Returns the emitted sets."""
+    cand = list(range(len(skq_levels[L - 1])))
+    emitted = [None] * L
+    for l in range(L - 1, -1, -1):
+        emitted[l] = sorted(cand)
+        if l == 0:
+            break
+        stream = [(float(sq[l][i]), i) for sq in sqk_levels_heads for i in cand]
+        stream += [(float(skq_levels[l][i]), i) for i in cand]
+        stream.sort(key=lambda t: (-t[0], t[1]))
+        parents, seen = [], set()
+        for _, i in stream:
+            if len(parents) >= k:
+                break
+            if i not in seen:
+                seen.add(i)
+                parents.append(i)
+        cand = sorted(p * i + r for i in parents for r in range(p))
+    return emitted
+
+
+def level_scores_fsum(x, p, L):
+    """Eqs. score-base / score-pool without the oracle: exact sum of squares (math.fsum), fp64
+    sqrt, rounded to fp32, then max over each window. Returns one array per level."""
+    s0 = np.array([np.float32(math.sqrt(math.fsum(float(t) * float(t) for t in row))) for row in x],
+                  np.float32)
+    out = [s0]
+    for l in range(1, L):
+        w = p ** l
+        out.append(s0.reshape(-1, w).max(axis=1))
+    return out
