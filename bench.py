@@ -34,19 +34,24 @@ PEAK_HBM_GBS = 8000.0
 
 
 def stage_work(pr, S, Ptot, es):
-    """Algorithmic bytes / flops per call of every stage (stage boundaries materialised)."""
+    """Algorithmic bytes / flops per call of every stage (stage boundaries materialised). With
+    one selection per KV group (Hs = Hkv selection heads) idx, slot, K~, V~, dK~, dV~ are per
+    group; Q~, O~ and their gradients stay per query head."""
     B, N, Hq, Hkv, D = pr.B, pr.N, pr.Hq, pr.Hkv, pr.D
+    Hs = Hkv if pr.flags & 4 else Hq
     R = Ptot - N
     BH = B * Hq
+    BS = B * Hs
     sdpa_pairs = B * Hq * S * (S + 1) / 2  # causal (query, key) pairs
     return {
         # read Q, K, V once; write levels 1..L-1 and the fp32 scores
         "pool_score": ("hbm", (Hq + 2 * Hkv) * B * N * D * es + (Hq + 2 * Hkv) * B * R * D * es
                        + (Hq + Hkv) * B * Ptot * 4),
-        # read both score streams of the candidates, write idx and the slot map
-        "select": ("hbm", BH * (2 * 4 * (S + 0) + 4 * S + 4 * Ptot)),
-        # read S rows of Q, K, V (pyramid or input) and write them
-        "gather": ("hbm", 6 * BH * S * D * es),
+        # read the score streams of the candidates (Hq / Hs query streams and the KV stream per
+        # selection), write idx and the slot map
+        "select": ("hbm", BS * ((Hq // Hs + 1) * 4 * S + 4 * S + 4 * Ptot)),
+        # read S rows of Q (per query head) and of K, V (per selection head) and write them
+        "gather": ("hbm", 2 * (BH + 2 * BS) * S * D * es),
         "sdpa_fwd": ("mfma", 4 * sdpa_pairs * D),
         # read S rows of Otilde, write N rows of O
         "scatter": ("hbm", BH * (S + N) * D * es),
@@ -54,8 +59,8 @@ def stage_work(pr, S, Ptot, es):
         "scatter_bwd": ("hbm", BH * (S + N) * D * es),
         # dV = P^T dO, dP = dO V^T, dK = dS^T Q, dQ = dS K
         "sdpa_bwd": ("mfma", 8 * sdpa_pairs * D),
-        # read S rows of dQ~, dK~, dV~; write dQ, dK, dV
-        "gather_bwd": ("hbm", 3 * BH * S * D * es + B * (Hq + 2 * Hkv) * N * D * es),
+        # read S rows of dQ~ (per query head) and dK~, dV~ (per selection head); write dQ, dK, dV
+        "gather_bwd": ("hbm", (BH + 2 * BS) * S * D * es + B * (Hq + 2 * Hkv) * N * D * es),
     }
 
 
@@ -97,7 +102,7 @@ def run_gpu(args, cfg):
     q, k, v, dout = inp["q"], inp["k"], inp["v"], inp["dout"]
     B, N, Hq, D = q.shape
     Hkv = k.shape[2]
-    pr = lh.problem(B, N, Hq, Hkv, D, cfg.p, cfg.L, cfg.k, q.dtype)
+    pr = lh.problem(B, N, Hq, Hkv, D, cfg.p, cfg.L, cfg.k, q.dtype, flags=cfg.flags)
     if lh.lh_check(pr) != lh.LH_OK:
         raise SystemExit(f"invalid problem: {lh.lh_last_error()}")
     S, Ptot = lh.lh_subseq_len(pr), lh.lh_pyramid_rows(pr)
@@ -105,9 +110,11 @@ def run_gpu(args, cfg):
     dt = q.dtype
     es = q.element_size()
     o = torch.empty_like(q)
-    idx = torch.empty(B, Hq, S, dtype=torch.int32, device=dev)
-    slot = torch.empty(B, Hq, Ptot, dtype=torch.int32, device=dev)
-    qs, ks, vs, os_ = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(4))
+    Hs = lh.selection_heads(pr)
+    idx = torch.empty(B, Hs, S, dtype=torch.int32, device=dev)
+    slot = torch.empty(B, Hs, Ptot, dtype=torch.int32, device=dev)
+    qs, os_ = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(2))
+    ks, vs = (torch.empty(B, Hs, S, D, dtype=dt, device=dev) for _ in range(2))
     lse = torch.empty(B, Hq, S, dtype=torch.float32, device=dev)
     dq = torch.empty_like(q)
     dk = torch.empty_like(k)
@@ -124,7 +131,8 @@ def run_gpu(args, cfg):
         # one forward (state for the backward), the adjoint of the scatter, then exactly one call
         # of the SDPA backward, then a plain streaming kernel of known size for the counter scale
         lh.lh_attention_fwd(pr, q, k, v, o, idx, slot, qs, ks, vs, os_, lse, wsf, stream=stream)
-        dos1, dqs1, dks1, dvs1 = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(4))
+        dos1, dqs1 = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(2))
+        dks1, dvs1 = (torch.empty(B, Hs, S, D, dtype=dt, device=dev) for _ in range(2))
         wsd1 = lh.workspace(pr, lh.LH_OP_SDPA_BWD, dev)
         lh.lh_scatter_bwd(pr, dout, slot, dos1, stream=stream)
         torch.cuda.synchronize()
@@ -165,7 +173,8 @@ def run_gpu(args, cfg):
     skq = torch.empty(B, Hkv, Ptot, dtype=torch.float32, device=dev)
     wss = lh.workspace(pr, lh.LH_OP_SELECT, dev)
     wsd = lh.workspace(pr, lh.LH_OP_SDPA_BWD, dev)
-    dos, dqs, dks, dvs = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(4))
+    dos, dqs = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(2))
+    dks, dvs = (torch.empty(B, Hs, S, D, dtype=dt, device=dev) for _ in range(2))
     stages = {
         "pool_score": lambda: lh.lh_pool_score(pr, q, k, v, qp, kp, vp, sqk, skq, stream=stream),
         "select": lambda: lh.lh_select_topk(pr, sqk, skq, idx, slot, wss, stream=stream),
@@ -292,6 +301,8 @@ def main():
     ap.add_argument("--config", default="c4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=512)
+    ap.add_argument("--gqa-shared", action="store_true",
+                    help="one selection per KV group (LH_FLAG_GQA_SHARED) instead of one per query head")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="run one SDPA backward call and one copy kernel (for rocprofv3 --pmc), then exit")
     args = ap.parse_args()
@@ -302,6 +313,8 @@ def main():
               file=sys.stderr)
         raise SystemExit(2)
     cfg = workloads.CONFIGS[args.config]
+    if args.gqa_shared:
+        cfg = workloads.scaled(cfg, name=cfg.name + "-gqa-shared", flags=cfg.flags | 4)
     if args.traffic_probe:
         run_gpu(args, cfg)
         return
@@ -315,7 +328,8 @@ def main():
         dtype="bf16" if cfg.dtype == "bf16" else "f32", data="synthetic",
         config=dict(workload=(f"lighthouse layer fwd+bwd {cfg.name}: B={cfg.B} N={cfg.N} Hq={cfg.Hq} "
                               f"Hkv={cfg.Hkv} D={cfg.D} p={cfg.p} L={cfg.L} k={cfg.k} S={summary['S']} "
-                              f"{cfg.dtype}, {cfg.structure} inputs"),
+                              f"{cfg.dtype}, {cfg.structure} inputs"
+                              + (", one selection per KV group" if cfg.flags & 4 else "")),
                     global_batch=cfg.B, seq_len=cfg.N, parallelism="single-gpu"),
         roofline=roof,
         summary=summary,

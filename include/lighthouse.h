@@ -91,7 +91,15 @@ enum {
      [s, e) keeps its best floor(k e / #cand) - floor(k s / #cand) candidates by the same key
      and tie-break. Every chunk of the sequence contributes its share, the level still keeps
      k parents, and S and every shape are those of the exact mode. */
-  LH_FLAG_STRATIFIED = 1u << 1
+  LH_FLAG_STRATIFIED = 1u << 1,
+  /* One selection per KV group (GQA-shared), a reading beyond the paper's MHA model: the
+     group's query score of an entry is the max of its query heads' scores (Eq. score-pool), and
+     it is combined with the KV head's score by the max of Eq. topk. idx [B,Hkv,S] and slot
+     [B,Hkv,Ptot] are then per KV head, as are ks, vs (and dks, dvs); every query head of the
+     group gathers its q rows with the group's idx and attends over the group's ks, vs, and the
+     group's dks, dvs sum over its query heads. Without the flag (default) every query head
+     selects on its own (the tensors above are per query head). */
+  LH_FLAG_GQA_SHARED = 1u << 2
 };
 
 /* workspace owners for lh_workspace_bytes */
@@ -140,6 +148,8 @@ const char* lh_status_str(lh_status s);
 const char* lh_last_error(void);
 
 /* ---------------- stage entry points (asynchronous on `stream`) ---------------- */
+/* Hs below is the number of selection heads: Hq, or Hkv with LH_FLAG_GQA_SHARED; query head hq
+   uses selection head hq / (Hq / Hs). */
 
 /* Sec. 3.3, Eq. pool: level-l entry i is the mean of base rows i p^l .. (i+1) p^l - 1, for
    l = 1..L-1 (level 0 is the input itself and is not copied). Writes qpyr, kpyr, vpyr. */
@@ -157,28 +167,31 @@ lh_status lh_score(const lh_problem* pr, const void* q, const void* k,
 lh_status lh_pool_score(const lh_problem* pr, const void* q, const void* k, const void* v,
                         void* qpyr, void* kpyr, void* vpyr, float* s_qk, float* s_kq, void* stream);
 
-/* Sec. 3.4 (Eq. topk, Fig. 2 panel 3) and Sec. 3.5 (causal order): per (b, hq), the
-   per-level descent described at the top of this file, then the causal ordering.
-   Writes idx [B,Hq,S] and slot [B,Hq,Ptot] (-1 for entries not gathered).
+/* Sec. 3.4 (Eq. topk, Fig. 2 panel 3) and Sec. 3.5 (causal order): per (b, selection head),
+   the per-level descent described at the top of this file, then the causal ordering.
+   Writes idx [B,Hs,S] and slot [B,Hs,Ptot] (-1 for entries not gathered).
    ws: device workspace of at least lh_workspace_bytes(LH_OP_SELECT) bytes. */
 lh_status lh_select_topk(const lh_problem* pr, const float* s_qk, const float* s_kq,
                          int32_t* idx, int32_t* slot, void* ws, size_t ws_bytes, void* stream);
 
 /* Sec. 3.5 (gather equation): qs[b,hq,m] = Q^(l_m)[b, i_m, hq], ks/vs likewise from KV head
-   hq/(Hq/Hkv), where idx[b,hq,m] = off_{l_m} + i_m. Ids below N read q/k/v, the rest read the
-   pyramid buffers. Bitwise copies. */
+   hq/(Hq/Hkv), where idx[b,hs,m] = off_{l_m} + i_m for the selection head hs of hq. Ids below N
+   read q/k/v, the rest read the pyramid buffers. Bitwise copies. qs is [B,Hq,S,D]; ks and vs
+   are [B,Hs,S,D] (per selection head). */
 lh_status lh_gather(const lh_problem* pr, const void* q, const void* k, const void* v,
                     const void* qpyr, const void* kpyr, const void* vpyr, const int32_t* idx,
                     void* qs, void* ks, void* vs, void* stream);
 
 /* Sec. 3.5, Eq. attn-sub with Eq. sdpa: os = softmax(scale qs ks^T + causal mask) vs per
-   (b, hq) over the S gathered rows; lse = natural-log row log-sum-exp of the scaled,
-   masked logits (fp32). Accumulation in fp32 (MFMA for bf16). */
+   (b, hq) over the S gathered rows (ks, vs of the selection head of hq); lse = natural-log row
+   log-sum-exp of the scaled, masked logits (fp32). Accumulation in fp32 (MFMA for bf16).
+   os [B,Hq,S,D], lse [B,Hq,S]. */
 lh_status lh_sdpa_fwd(const lh_problem* pr, const void* qs, const void* ks, const void* vs,
                       void* os, float* lse, void* stream);
 
 /* Gradient of lh_sdpa_fwd (App. C.4: gradients flow through the gathered values):
-   given dos = dL/dos, writes dqs, dks, dvs. Uses lse saved by the forward.
+   given dos = dL/dos, writes dqs [B,Hq,S,D] and dks, dvs [B,Hs,S,D] (the gradients of a
+   selection head's rows summed over its query heads). Uses lse saved by the forward.
    ws: at least lh_workspace_bytes(LH_OP_SDPA_BWD) bytes. Deterministic. */
 lh_status lh_sdpa_bwd(const lh_problem* pr, const void* qs, const void* ks, const void* vs,
                       const void* os, const float* lse, const void* dos,
@@ -187,7 +200,8 @@ lh_status lh_sdpa_bwd(const lh_problem* pr, const void* qs, const void* ks, cons
 /* Sec. 3.6, Eqs. fanout and scatter: entry (l, i) at position m writes os[m] to base
    positions R(l,i) = [(i+1) p^l - 1, (i+2) p^l - 2] (clipped at N-1); contributions of
    different levels are summed in fp32 (level L-1 first) and rounded once. Base positions
-   with no contributor get 0. Writes o [B,N,Hq,D]. */
+   with no contributor get 0. Query head hq reads the slot row of its selection head.
+   Writes o [B,N,Hq,D]. */
 lh_status lh_scatter(const lh_problem* pr, const void* os, const int32_t* slot,
                      void* o, void* stream);
 
@@ -198,8 +212,9 @@ lh_status lh_scatter_bwd(const lh_problem* pr, const void* dout, const int32_t* 
 
 /* Adjoint of lh_gather followed by the adjoint of lh_pyramid_pool:
    dq[b,j,hq] = sum_l dqs[slot(l, floor(j/p^l))] / p^l over gathered entries;
-   dk[b,j,g], dv[b,j,g] are the same sums, also over the query heads of group g.
-   fp32 accumulation, one rounding. Writes dq, dk, dv. */
+   dk[b,j,g], dv[b,j,g] are the same sums over the selection heads of group g (its query
+   heads; the group itself with LH_FLAG_GQA_SHARED). fp32 accumulation, one rounding.
+   Writes dq, dk, dv. */
 lh_status lh_gather_bwd(const lh_problem* pr, const void* dqs, const void* dks, const void* dvs,
                         const int32_t* slot, void* dq, void* dk, void* dv, void* stream);
 

@@ -14,7 +14,7 @@ import os
 import torch
 
 __all__ = [
-    "LH_OK", "LH_F32", "LH_BF16", "LH_FLAG_REPLACE_PARENTS", "LH_FLAG_STRATIFIED", "LH_OP_SELECT", "LH_OP_SDPA_BWD",
+    "LH_OK", "LH_F32", "LH_BF16", "LH_FLAG_REPLACE_PARENTS", "LH_FLAG_STRATIFIED", "LH_FLAG_GQA_SHARED", "LH_OP_SELECT", "LH_OP_SDPA_BWD",
     "LH_OP_ATTENTION_FWD", "LH_OP_ATTENTION_BWD", "LH_OP_ATTENTION_FWD_INDEXED", "LighthouseError", "lh_problem", "problem",
     "lh_check", "lh_level_rows", "lh_level_offset", "lh_pyramid_rows", "lh_subseq_len",
     "lh_workspace_bytes", "lh_status_str", "lh_last_error", "lh_pyramid_pool", "lh_score",
@@ -22,6 +22,7 @@ __all__ = [
     "lh_scatter_bwd", "lh_gather_bwd", "lh_attention_fwd", "lh_attention_bwd", "lh_sdpa_fwd_indexed",
     "lh_sdpa_bwd_indexed", "lh_attention_fwd_indexed", "lh_attention_bwd_indexed", "workspace",
     "attention_forward", "attention_backward", "attention_forward_indexed", "attention_backward_indexed",
+    "selection_heads",
     "library_path", "EXPORTED",
 ]
 
@@ -29,6 +30,7 @@ LH_OK = 0
 LH_F32, LH_BF16 = 0, 1
 LH_FLAG_REPLACE_PARENTS = 1
 LH_FLAG_STRATIFIED = 2
+LH_FLAG_GQA_SHARED = 4
 LH_OP_SELECT, LH_OP_SDPA_BWD, LH_OP_ATTENTION_FWD, LH_OP_ATTENTION_BWD, LH_OP_ATTENTION_FWD_INDEXED = 0, 1, 2, 3, 4
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -260,6 +262,11 @@ def lh_attention_bwd_indexed(pr, q, k, v, qpyr, kpyr, vpyr, idx, slot, os_, lse,
 
 # ---------------------------------------------------------------- allocation helpers
 
+def selection_heads(pr) -> int:
+    """Heads of idx, slot, ks, vs (and dks, dvs): Hkv with LH_FLAG_GQA_SHARED, else Hq."""
+    return pr.Hkv if pr.flags & LH_FLAG_GQA_SHARED else pr.Hq
+
+
 def workspace(pr, op, device="cuda"):
     """A device byte buffer of lh_workspace_bytes(pr, op) bytes (None if zero)."""
     n = lh_workspace_bytes(pr, op)
@@ -276,14 +283,15 @@ def attention_forward(q, k, v, p, L, k_budget, scale=0.0, flags=0, stream=None):
     if st != LH_OK:
         raise LighthouseError(f"lh_check: {lh_status_str(st)}: {lh_last_error()}")
     S, Ptot = lh_subseq_len(pr), lh_pyramid_rows(pr)
+    Hs = selection_heads(pr)
     dev = q.device
     out = dict(
         o=torch.empty_like(q),
-        idx=torch.empty(B, Hq, S, dtype=torch.int32, device=dev),
-        slot=torch.empty(B, Hq, Ptot, dtype=torch.int32, device=dev),
+        idx=torch.empty(B, Hs, S, dtype=torch.int32, device=dev),
+        slot=torch.empty(B, Hs, Ptot, dtype=torch.int32, device=dev),
         qs=torch.empty(B, Hq, S, D, dtype=q.dtype, device=dev),
-        ks=torch.empty(B, Hq, S, D, dtype=q.dtype, device=dev),
-        vs=torch.empty(B, Hq, S, D, dtype=q.dtype, device=dev),
+        ks=torch.empty(B, Hs, S, D, dtype=q.dtype, device=dev),
+        vs=torch.empty(B, Hs, S, D, dtype=q.dtype, device=dev),
         os=torch.empty(B, Hq, S, D, dtype=q.dtype, device=dev),
         lse=torch.empty(B, Hq, S, dtype=torch.float32, device=dev),
     )
@@ -304,12 +312,13 @@ def attention_forward_indexed(q, k, v, p, L, k_budget, scale=0.0, flags=0, strea
     if st != LH_OK:
         raise LighthouseError(f"lh_check: {lh_status_str(st)}: {lh_last_error()}")
     S, Ptot = lh_subseq_len(pr), lh_pyramid_rows(pr)
+    Hs = selection_heads(pr)
     R = max(Ptot - N, 1)
     dev = q.device
     out = dict(
         o=torch.empty_like(q),
-        idx=torch.empty(B, Hq, S, dtype=torch.int32, device=dev),
-        slot=torch.empty(B, Hq, Ptot, dtype=torch.int32, device=dev),
+        idx=torch.empty(B, Hs, S, dtype=torch.int32, device=dev),
+        slot=torch.empty(B, Hs, Ptot, dtype=torch.int32, device=dev),
         qpyr=torch.empty(B, R, Hq, D, dtype=q.dtype, device=dev),
         kpyr=torch.empty(B, R, Hkv, D, dtype=q.dtype, device=dev),
         vpyr=torch.empty(B, R, Hkv, D, dtype=q.dtype, device=dev),

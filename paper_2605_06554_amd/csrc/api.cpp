@@ -34,7 +34,7 @@ lh_status make_shape(const lh_problem* pr, LhShape* s) {
   if (pr->L > 1 && pr->p < 2) return fail(LH_E_PARAM, "pooling factor p must be >= 2 when L > 1 (p=%d)", pr->p);
   if (pr->k < 0) return fail(LH_E_PARAM, "budget k must be >= 0 (k=%d)", pr->k);
   if (pr->dtype != LH_F32 && pr->dtype != LH_BF16) return fail(LH_E_DTYPE, "dtype must be LH_F32 or LH_BF16 (%d)", pr->dtype);
-  if (pr->flags & ~(uint32_t)(LH_FLAG_REPLACE_PARENTS | LH_FLAG_STRATIFIED))
+  if (pr->flags & ~(uint32_t)(LH_FLAG_REPLACE_PARENTS | LH_FLAG_STRATIFIED | LH_FLAG_GQA_SHARED))
     return fail(LH_E_PARAM, "unknown flag bits 0x%x", pr->flags);
   if (!(pr->scale == pr->scale) || isinf(pr->scale)) return fail(LH_E_PARAM, "scale must be finite");
   memset(s, 0, sizeof(*s));
@@ -43,6 +43,9 @@ lh_status make_shape(const lh_problem* pr, LhShape* s) {
   s->Hq = pr->Hq;
   s->Hkv = pr->Hkv;
   s->G = pr->Hq / pr->Hkv;
+  const bool shared = (pr->flags & LH_FLAG_GQA_SHARED) != 0;
+  s->Hs = shared ? pr->Hkv : pr->Hq;
+  s->Gq = shared ? s->G : 1;
   s->D = pr->D;
   s->p = pr->L > 1 ? pr->p : (pr->p >= 1 ? pr->p : 1);
   s->L = pr->L;
@@ -101,7 +104,7 @@ FwdWs fwd_ws(const LhShape& s) {
   w.vpyr = o, o += align256((size_t)s.B * s.R * s.Hkv * s.D * es);
   w.s_qk = o, o += align256((size_t)s.B * s.Hq * s.Ptot * 4);
   w.s_kq = o, o += align256((size_t)s.B * s.Hkv * s.Ptot * 4);
-  w.sel = o, o += align256((size_t)s.B * s.Hq * s.Scand * 4);
+  w.sel = o, o += align256((size_t)s.B * s.Hs * s.Scand * 4);
   w.total = o;
   return w;
 }
@@ -112,10 +115,11 @@ BwdWs bwd_ws(const LhShape& s) {
   BwdWs w;
   size_t o = 0;
   const size_t t = align256((size_t)s.B * s.Hq * s.S * s.D * esize(s));
+  const size_t tkv = align256((size_t)s.B * s.Hs * s.S * s.D * esize(s));  // per selection head
   w.dos = o, o += t;
   w.dqs = o, o += t;
-  w.dks = o, o += t;
-  w.dvs = o, o += t;
+  w.dks = o, o += tkv;
+  w.dvs = o, o += tkv;
   w.delta = o, o += align256((size_t)s.B * s.Hq * s.S * 4);
   w.total = o;
   return w;
@@ -123,7 +127,7 @@ BwdWs bwd_ws(const LhShape& s) {
 
 size_t ws_bytes(const LhShape& s, int op) {
   switch (op) {
-    case LH_OP_SELECT: return align256((size_t)s.B * s.Hq * s.Scand * 4);
+    case LH_OP_SELECT: return align256((size_t)s.B * s.Hs * s.Scand * 4);
     case LH_OP_SDPA_BWD: return align256((size_t)s.B * s.Hq * s.S * 4);
     case LH_OP_ATTENTION_FWD: return fwd_ws(s).total;
     case LH_OP_ATTENTION_BWD: return bwd_ws(s).total;

@@ -76,6 +76,7 @@ struct GatherArgs {
   void *qs, *ks, *vs;
   int64_t N, R, S;
   int32_t Hq, Hkv, G, D, cpr_shift, rows_per_block;
+  int32_t Hs, Gq;  // selection heads, query heads per selection head
 };
 
 template <typename T>
@@ -88,13 +89,20 @@ __global__ void __launch_bounds__(256) gather_kernel(GatherArgs a) {
   const int hq = (int)(bh % a.Hq);
   const int64_t b = bh / a.Hq;
   const int g = hq / a.G;
-  const int64_t id = a.idx[bh * a.S + m];
+  // rows of the selection head of hq; K~ and V~ are written once per selection head (by its
+  // first query head), Q~ per query head
+  const int64_t bs = b * a.Hs + hq / a.Gq;
+  const bool kv_out = hq % a.Gq == 0;
+  const int64_t id = a.idx[bs * a.S + m];
   const int64_t o = (bh * a.S + m) * a.D + cc * CH;
+  const int64_t okv = (bs * a.S + m) * a.D + cc * CH;
   if (id < 0 || id >= a.N + a.R) {  // not a pyramid id: zero row, never an out-of-range read
     const u32x4 z{0, 0, 0, 0};
     *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.qs) + o) = z;
-    *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.ks) + o) = z;
-    *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.vs) + o) = z;
+    if (kv_out) {
+      *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.ks) + okv) = z;
+      *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.vs) + okv) = z;
+    }
     return;
   }
   const T *sq, *sk, *sv;
@@ -109,11 +117,13 @@ __global__ void __launch_bounds__(256) gather_kernel(GatherArgs a) {
     sv = reinterpret_cast<const T*>(a.vp) + ((b * a.R + r) * a.Hkv + g) * a.D;
   }
   const u32x4 xq = load_raw(sq + cc * CH);
-  const u32x4 xk = load_raw(sk + cc * CH);
-  const u32x4 xv = load_raw(sv + cc * CH);
   *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.qs) + o) = xq;
-  *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.ks) + o) = xk;
-  *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.vs) + o) = xv;
+  if (kv_out) {
+    const u32x4 xk = load_raw(sk + cc * CH);
+    const u32x4 xv = load_raw(sv + cc * CH);
+    *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.ks) + okv) = xk;
+    *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.vs) + okv) = xv;
+  }
 }
 
 // ---------------------------------------------------------------- scatter and gather_bwd
@@ -124,7 +134,8 @@ struct RunArgs {
   void* dst;            // [B, N, H, D]
   int64_t Ptot;
   int32_t N, S, D, nruns, run;        // run = positions per run: p (1 when L = 1)
-  int32_t Hq, H, Gs, HC, cpr_shift;   // output head h sums query heads h Gs .. h Gs + Gs - 1
+  int32_t Hq, H, Gs, HC, cpr_shift;   // output head h sums source heads h Gs .. h Gs + Gs - 1
+  int32_t Hsrc, Hslot, sdiv;          // heads of src and of slot; source head x uses slot head x / sdiv
   int32_t pshift;                     // log2 p when p is a power of two, else -1
   int32_t pw[16];                     // p^l
   int32_t off[17];                    // flattened id of entry (l, 0)
@@ -132,6 +143,12 @@ struct RunArgs {
   int32_t vec_slots;                  // Ptot % 4 == 0: a head's slot row is 16-byte aligned
   float inv[16];                      // 1 / p^l
 };
+
+// Row 0 of source head x of batch b in src, and its slot row.
+__device__ __forceinline__ int64_t src_head(const RunArgs& a, int64_t b, int x) { return b * a.Hsrc + x; }
+__device__ __forceinline__ const int32_t* slot_row(const RunArgs& a, int64_t b, int x) {
+  return a.slot + (b * a.Hslot + x / a.sdiv) * a.Ptot;
+}
 
 // Level-l entry (l >= 1) shared by every position of run c: floor(c / p^(l-1)).
 __device__ __forceinline__ int32_t run_entry(const RunArgs& a, uint32_t c, int l) {
@@ -148,9 +165,8 @@ __global__ void __launch_bounds__(256) scatter_kernel(RunArgs a) {
   if (c >= (uint32_t)a.nruns || hc >= a.HC) return;
   const int hq = hc >> a.cpr_shift, cc = hc & ((1 << a.cpr_shift) - 1);
   const int64_t b = blockIdx.z;
-  const int64_t bh = b * a.Hq + hq;
-  const int32_t* sl = a.slot + bh * a.Ptot;
-  const T* src = reinterpret_cast<const T*>(a.src) + bh * a.S * a.D + cc * CH;
+  const int32_t* sl = slot_row(a, b, hq);
+  const T* src = reinterpret_cast<const T*>(a.src) + src_head(a, b, hq) * a.S * a.D + cc * CH;
   float acc[CH];
 #pragma unroll
   for (int e = 0; e < CH; ++e) acc[e] = 0.0f;
@@ -169,8 +185,8 @@ __global__ void __launch_bounds__(256) scatter_kernel(RunArgs a) {
     for (int l = L - 1; l >= 1; --l) add_chunk<T>(acc, v[l]);
   }
   // level 0: position j takes entry (0, j)
-  T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.Hq + hq) * (int64_t)a.D + cc * CH;
-  const int64_t dstride = (int64_t)a.Hq * a.D;
+  T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.H + hq) * (int64_t)a.D + cc * CH;
+  const int64_t dstride = (int64_t)a.H * a.D;
   const int32_t jbase = (int32_t)(c * (uint32_t)a.run) - 1;
   if constexpr (PU > 0) {
     int32_t m0[PU];
@@ -235,9 +251,9 @@ __global__ void __launch_bounds__(256) gather_bwd_kernel(RunArgs a) {
   T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.H + h) * (int64_t)a.D + cc * CH;
   const int64_t dstride = (int64_t)a.H * a.D;
   for (int g = 0; g < a.Gs; ++g) {
-    const int64_t bhq = b * a.Hq + (int64_t)h * a.Gs + g;
-    const int32_t* sl = a.slot + bhq * a.Ptot;
-    const T* src = reinterpret_cast<const T*>(a.src) + bhq * a.S * a.D + cc * CH;
+    const int x = h * a.Gs + g;
+    const int32_t* sl = slot_row(a, b, x);
+    const T* src = reinterpret_cast<const T*>(a.src) + src_head(a, b, x) * a.S * a.D + cc * CH;
     int32_t m[L > 1 ? L : 2];
 #pragma unroll
     for (int l = L - 1; l >= 1; --l) m[l] = sl[ent[l]];
@@ -280,10 +296,11 @@ __global__ void __launch_bounds__(256) gather_bwd_kernel(RunArgs a) {
 #pragma unroll
       for (int e = 0; e < CH; ++e) o[e] = 0.0f;
       for (int g = 0; g < a.Gs; ++g) {
-        const int64_t bhq = b * a.Hq + (int64_t)h * a.Gs + g;
-        const int32_t m0 = a.slot[bhq * a.Ptot + jbase + r];
+        const int x = h * a.Gs + g;
+        const int32_t m0 = slot_row(a, b, x)[jbase + r];
         if ((uint32_t)m0 < (uint32_t)a.S)
-          add_chunk<T>(o, load_raw(reinterpret_cast<const T*>(a.src) + (bhq * a.S + m0) * a.D + cc * CH));
+          add_chunk<T>(o, load_raw(reinterpret_cast<const T*>(a.src) + (src_head(a, b, x) * a.S + m0) * a.D +
+                                   cc * CH));
       }
 #pragma unroll
       for (int e = 0; e < CH; ++e) o[e] = acc[e] + o[e];
@@ -352,9 +369,8 @@ __global__ void __launch_bounds__(256) scatter_long_kernel(RunArgs a) {
   if (c >= (uint32_t)a.nruns || hc >= a.HC) return;
   const int hq = hc >> a.cpr_shift, cc = hc & ((1 << a.cpr_shift) - 1);
   const int64_t b = blockIdx.z;
-  const int64_t bh = b * a.Hq + hq;
-  const int32_t* sl = a.slot + bh * a.Ptot;
-  const T* src = reinterpret_cast<const T*>(a.src) + bh * a.S * a.D + cc * CH;
+  const int32_t* sl = slot_row(a, b, hq);
+  const T* src = reinterpret_cast<const T*>(a.src) + src_head(a, b, hq) * a.S * a.D + cc * CH;
   const int32_t j0 = (int32_t)(c * RL) - 1;
   int32_t msh[NSH > 0 ? NSH : 1], msub[NSUB > 0 ? NSUB : 1], m0[RL];
 #pragma unroll
@@ -382,8 +398,8 @@ __global__ void __launch_bounds__(256) scatter_long_kernel(RunArgs a) {
   for (int e = 0; e < CH; ++e) acc[e] = 0.0f;
 #pragma unroll
   for (int l = L - 1; l >= LS; --l) add_chunk<T>(acc, vsh[l - LS]);
-  T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.Hq + hq) * (int64_t)a.D + cc * CH;
-  const int64_t dstride = (int64_t)a.Hq * a.D;
+  T* dst = reinterpret_cast<T*>(a.dst) + ((b * a.N) * a.H + hq) * (int64_t)a.D + cc * CH;
+  const int64_t dstride = (int64_t)a.H * a.D;
 #pragma unroll
   for (int r = 0; r < RL; ++r) {
     const int32_t j = j0 + r;
@@ -412,9 +428,8 @@ __global__ void __launch_bounds__(256) gather_bwd_long_kernel(RunArgs a) {
   if (c >= (uint32_t)a.nruns || hc >= a.HC) return;
   const int h = hc >> a.cpr_shift, cc = hc & ((1 << a.cpr_shift) - 1);
   const int64_t b = blockIdx.z;
-  const int64_t bh = b * a.Hq + h;
-  const int32_t* sl = a.slot + bh * a.Ptot;
-  const T* src = reinterpret_cast<const T*>(a.src) + bh * a.S * a.D + cc * CH;
+  const int32_t* sl = slot_row(a, b, h);
+  const T* src = reinterpret_cast<const T*>(a.src) + src_head(a, b, h) * a.S * a.D + cc * CH;
   const int32_t j0 = (int32_t)(c * RL);
   int32_t msh[NSH > 0 ? NSH : 1], msub[NSUB > 0 ? NSUB : 1], m0[RL];
 #pragma unroll
@@ -489,7 +504,7 @@ __global__ void __launch_bounds__(256) gather_bwd_group_kernel(RunArgs a) {
 #pragma unroll
     for (int gg = 0; gg < GB; ++gg) {
       const bool live = g0 + gg < a.Gs;
-      const int32_t* sl = a.slot + (b * a.Hq + (int64_t)h * a.Gs + g0 + gg) * a.Ptot;
+      const int32_t* sl = slot_row(a, b, h * a.Gs + g0 + gg);
 #pragma unroll
       for (int l = L - 1; l >= 1; --l) m[gg][l] = live ? sl[ent[l]] : -1;
 #pragma unroll
@@ -498,8 +513,7 @@ __global__ void __launch_bounds__(256) gather_bwd_group_kernel(RunArgs a) {
     u32x4 v[GB][LA], v0[GB][PU];
 #pragma unroll
     for (int gg = 0; gg < GB; ++gg) {
-      const T* src = reinterpret_cast<const T*>(a.src) +
-                     (b * a.Hq + (int64_t)h * a.Gs + g0 + gg) * a.S * a.D + cc * CH;
+      const T* src = reinterpret_cast<const T*>(a.src) + src_head(a, b, h * a.Gs + g0 + gg) * a.S * a.D + cc * CH;
 #pragma unroll
       for (int l = L - 1; l >= 1; --l) v[gg][l] = load_entry_row(src, m[gg][l], a.S, a.D, sizeof(T));
 #pragma unroll
@@ -571,9 +585,8 @@ __global__ void __launch_bounds__(256) gather_bwd_group_long_kernel(RunArgs a) {
     }
 #pragma unroll
   for (int r = 0; r < RH; ++r) sidx[NC + r] = j0 + r < a.N ? j0 + r : -1;
-  const int64_t bhq0 = b * a.Hq + (int64_t)h * a.Gs;
   auto load_slots = [&](int g, int32_t* m) __attribute__((always_inline)) {
-    const int32_t* sl = a.slot + (bhq0 + g) * a.Ptot;
+    const int32_t* sl = slot_row(a, b, h * a.Gs + g);
 #pragma unroll
     for (int e = 0; e < NE; ++e) m[e] = sidx[e] >= 0 ? sl[sidx[e]] : -1;
   };
@@ -589,7 +602,7 @@ __global__ void __launch_bounds__(256) gather_bwd_group_long_kernel(RunArgs a) {
   int32_t m[NE], mn[NE];
   load_slots(0, m);
   for (int g = 0; g < a.Gs; ++g) {
-    const T* src = reinterpret_cast<const T*>(a.src) + (bhq0 + g) * a.S * a.D + cc * CH;
+    const T* src = reinterpret_cast<const T*>(a.src) + src_head(a, b, h * a.Gs + g) * a.S * a.D + cc * CH;
     u32x4 v[NE];
 #pragma unroll
     for (int e = 0; e < NE; ++e) v[e] = load_entry_row(src, m[e], a.S, a.D, sizeof(T));
@@ -627,6 +640,7 @@ struct ScatterBwdArgs {
   void* dos;  // [B, Hq, S, D]
   int64_t Ptot;
   int32_t N, S, U, WR, Hq, D, HW, cpr_shift, p;  // U = N + p^(L-1): positions of the shifted sequence
+  int32_t Hs, Gq;  // query head hq reads the slot row of selection head hq / Gq
   int32_t off[17];
   int32_t nrows[16];  // N / p^l
   int32_t epb[16];    // WR / p^l: level-l windows per workgroup
@@ -651,7 +665,7 @@ __global__ void __launch_bounds__(256) scatter_bwd_kernel(ScatterBwdArgs a) {
   if (hq >= a.Hq) return;  // no barriers below
   const int64_t b = blockIdx.z;
   const int64_t bh = b * a.Hq + hq;
-  const int32_t* sl = a.slot + bh * a.Ptot;
+  const int32_t* sl = a.slot + (b * a.Hs + hq / a.Gq) * a.Ptot;
   T* dos = reinterpret_cast<T*>(a.dos) + bh * a.S * a.D + cc * CH;
   const T* src = reinterpret_cast<const T*>(a.dout) + (b * a.N * a.Hq + hq) * (int64_t)a.D + cc * CH;
   const int64_t sstride = (int64_t)a.Hq * a.D;
@@ -795,8 +809,10 @@ static void launch_run_kernel(bool scatter, const LhShape& s, const RunArgs& a, 
 #undef LH_RUN_CASE
 }
 
+// H output heads, each summing Gs consecutive source heads of the Hsrc in src; source head x
+// reads slot row x / sdiv (of the s.Hs selection heads).
 static RunArgs run_args(const LhShape& s, const void* src, const int32_t* slot, void* dst, int H, int Gs,
-                        bool scatter) {
+                        int Hsrc, int sdiv, bool scatter) {
   RunArgs a = {};
   a.src = src;
   a.slot = slot;
@@ -810,6 +826,9 @@ static RunArgs run_args(const LhShape& s, const void* src, const int32_t* slot, 
   a.Hq = s.Hq;
   a.H = H;
   a.Gs = Gs;
+  a.Hsrc = Hsrc;
+  a.Hslot = s.Hs;
+  a.sdiv = sdiv;
   const int es = s.dtype == LH_BF16 ? 2 : 4;
   a.cpr_shift = cpr_shift_of(s.D, es);
   a.HC = H << a.cpr_shift;
@@ -847,6 +866,8 @@ static hipError_t launch_scatter_bwd_T(const LhShape& s, const void* dout, const
   a.S = (int32_t)s.S;
   a.U = (int32_t)(s.N + s.P);
   a.Hq = s.Hq;
+  a.Hs = s.Hs;
+  a.Gq = s.Gq;
   a.D = s.D;
   a.p = s.p;
   a.cpr_shift = cpr_shift_of(s.D, (int)sizeof(T));
@@ -888,7 +909,7 @@ using namespace lh;
 hipError_t lh_launch_gather(const LhShape& s, const void* q, const void* k, const void* v,
                             const void* qpyr, const void* kpyr, const void* vpyr,
                             const int32_t* idx, void* qs, void* ks, void* vs, hipStream_t st) {
-  GatherArgs a{q, k, v, qpyr, kpyr, vpyr, idx, qs, ks, vs, s.N, s.R, s.S, s.Hq, s.Hkv, s.G, s.D, 0, 0};
+  GatherArgs a{q, k, v, qpyr, kpyr, vpyr, idx, qs, ks, vs, s.N, s.R, s.S, s.Hq, s.Hkv, s.G, s.D, 0, 0, s.Hs, s.Gq};
   const int es = s.dtype == LH_BF16 ? 2 : 4;
   a.cpr_shift = cpr_shift_of(s.D, es);
   a.rows_per_block = 256 >> a.cpr_shift;
@@ -900,7 +921,7 @@ hipError_t lh_launch_gather(const LhShape& s, const void* q, const void* k, cons
 
 hipError_t lh_launch_scatter(const LhShape& s, const void* os, const int32_t* slot, void* o,
                              hipStream_t st) {
-  const RunArgs a = run_args(s, os, slot, o, s.Hq, 1, true);
+  const RunArgs a = run_args(s, os, slot, o, s.Hq, 1, s.Hq, s.Gq, true);
   dim3 grid, block;
   run_grid(a, (int)s.B, &grid, &block);
   if (s.dtype == LH_BF16) launch_run_kernel<bf16_t>(true, s, a, grid, block, st);
@@ -920,8 +941,10 @@ hipError_t lh_launch_gather_bwd(const LhShape& s, const void* dqs, const void* d
   const void* srcs[3] = {dqs, dks, dvs};
   void* dsts[3] = {dq, dk, dv};
   for (int which = 0; which < 3; ++which) {
-    const RunArgs a = run_args(s, srcs[which], slot, dsts[which], which == 0 ? s.Hq : s.Hkv,
-                               which == 0 ? 1 : s.G, false);
+    // dQ: per query head, from dqs [B,Hq,S,D]. dK, dV: per KV head, summing the gradients of
+    // its G / Gq selection heads in dks, dvs [B,Hs,S,D] (its query heads, or the group itself).
+    const RunArgs a = which == 0 ? run_args(s, srcs[0], slot, dsts[0], s.Hq, 1, s.Hq, s.Gq, false)
+                                 : run_args(s, srcs[which], slot, dsts[which], s.Hkv, s.G / s.Gq, s.Hs, 1, false);
     dim3 grid, block;
     run_grid(a, (int)s.B, &grid, &block);
     if (s.dtype == LH_BF16) launch_run_kernel<bf16_t>(false, s, a, grid, block, st);

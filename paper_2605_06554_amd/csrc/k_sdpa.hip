@@ -47,10 +47,12 @@ constexpr int TT = 32;  // rows per LDS tile
 template <int D>
 __global__ void __launch_bounds__(RT) sdpa_fwd_f32(const float* __restrict__ Q, const float* __restrict__ K,
                                                    const float* __restrict__ V, float* __restrict__ O,
-                                                   float* __restrict__ LSE, int64_t S, float scale) {
+                                                   float* __restrict__ LSE, int64_t S, float scale, int Hq,
+                                                   int Hs, int Gq) {
   __shared__ float Ks[TT][D];
   __shared__ float Vs[TT][D];
   const int64_t bh = blockIdx.y;
+  const int64_t kvh = (bh / Hq) * Hs + (bh % Hq) / Gq;  // selection head: rows of ks, vs
   const int64_t nqt = (S + RT - 1) / RT;
   const int64_t q0 = (nqt - 1 - (int64_t)blockIdx.x) * RT;
   const int64_t myq = q0 + threadIdx.x;
@@ -66,8 +68,8 @@ __global__ void __launch_bounds__(RT) sdpa_fwd_f32(const float* __restrict__ Q, 
   for (int64_t k0 = 0; k0 < kend; k0 += TT) {
     for (int e = threadIdx.x; e < TT * D; e += RT) {
       const int64_t key = k0 + e / D;
-      Ks[e / D][e % D] = key < S ? K[(bh * S + key) * D + e % D] : 0.0f;
-      Vs[e / D][e % D] = key < S ? V[(bh * S + key) * D + e % D] : 0.0f;
+      Ks[e / D][e % D] = key < S ? K[(kvh * S + key) * D + e % D] : 0.0f;
+      Vs[e / D][e % D] = key < S ? V[(kvh * S + key) * D + e % D] : 0.0f;
     }
     __syncthreads();
     for (int t = 0; t < TT; ++t) {
@@ -94,10 +96,12 @@ template <int D>
 __global__ void __launch_bounds__(RT) sdpa_bwd_dq_f32(const float* __restrict__ Q, const float* __restrict__ K,
                                                       const float* __restrict__ V, const float* __restrict__ dO,
                                                       const float* __restrict__ LSE, const float* __restrict__ DELTA,
-                                                      float* __restrict__ dQ, int64_t S, float scale) {
+                                                      float* __restrict__ dQ, int64_t S, float scale, int Hq,
+                                                      int Hs, int Gq) {
   __shared__ float Ks[TT][D];
   __shared__ float Vs[TT][D];
   const int64_t bh = blockIdx.y;
+  const int64_t kvh = (bh / Hq) * Hs + (bh % Hq) / Gq;
   const int64_t nqt = (S + RT - 1) / RT;
   const int64_t q0 = (nqt - 1 - (int64_t)blockIdx.x) * RT;
   const int64_t myq = q0 + threadIdx.x;
@@ -114,8 +118,8 @@ __global__ void __launch_bounds__(RT) sdpa_bwd_dq_f32(const float* __restrict__ 
   for (int64_t k0 = 0; k0 < kend; k0 += TT) {
     for (int e = threadIdx.x; e < TT * D; e += RT) {
       const int64_t key = k0 + e / D;
-      Ks[e / D][e % D] = key < S ? K[(bh * S + key) * D + e % D] : 0.0f;
-      Vs[e / D][e % D] = key < S ? V[(bh * S + key) * D + e % D] : 0.0f;
+      Ks[e / D][e % D] = key < S ? K[(kvh * S + key) * D + e % D] : 0.0f;
+      Vs[e / D][e % D] = key < S ? V[(kvh * S + key) * D + e % D] : 0.0f;
     }
     __syncthreads();
     for (int t = 0; t < TT; ++t) {
@@ -141,11 +145,12 @@ __global__ void __launch_bounds__(RT) sdpa_bwd_dkdv_f32(const float* __restrict_
                                                         const float* __restrict__ V, const float* __restrict__ dO,
                                                         const float* __restrict__ LSE, const float* __restrict__ DELTA,
                                                         float* __restrict__ dK, float* __restrict__ dV, int64_t S,
-                                                        float scale) {
+                                                        float scale, int Hq, int Hs, int Gq) {
   __shared__ float Qs[TT][D];
   __shared__ float dOs[TT][D];
   __shared__ float ls[TT], dls[TT];
-  const int64_t bh = blockIdx.y;
+  const int64_t bs = blockIdx.y;  // selection head: its keys gather the gradients of its Gq query heads
+  const int64_t bh = bs;
   const int64_t k0 = (int64_t)blockIdx.x * RT;
   const int64_t myk = k0 + threadIdx.x;
   float kr[D], vr[D], dk[D], dv[D];
@@ -154,15 +159,17 @@ __global__ void __launch_bounds__(RT) sdpa_bwd_dkdv_f32(const float* __restrict_
     vr[c] = myk < S ? V[(bh * S + myk) * D + c] : 0.0f;
     dk[c] = dv[c] = 0.0f;
   }
+  for (int mq = 0; mq < Gq; ++mq)
   for (int64_t qt = k0; qt < S; qt += TT) {
+    const int64_t bq = (bs / Hs) * Hq + (bs % Hs) * Gq + mq;  // member query head
     for (int e = threadIdx.x; e < TT * D; e += RT) {
       const int64_t q = qt + e / D;
-      Qs[e / D][e % D] = q < S ? Q[(bh * S + q) * D + e % D] : 0.0f;
-      dOs[e / D][e % D] = q < S ? dO[(bh * S + q) * D + e % D] : 0.0f;
+      Qs[e / D][e % D] = q < S ? Q[(bq * S + q) * D + e % D] : 0.0f;
+      dOs[e / D][e % D] = q < S ? dO[(bq * S + q) * D + e % D] : 0.0f;
     }
     for (int e = threadIdx.x; e < TT; e += RT) {
-      ls[e] = qt + e < S ? LSE[bh * S + qt + e] : 0.0f;
-      dls[e] = qt + e < S ? DELTA[bh * S + qt + e] : 0.0f;
+      ls[e] = qt + e < S ? LSE[bq * S + qt + e] : 0.0f;
+      dls[e] = qt + e < S ? DELTA[bq * S + qt + e] : 0.0f;
     }
     __syncthreads();
     for (int t = 0; t < TT; ++t) {
@@ -203,8 +210,10 @@ hipError_t lh_launch_sdpa_fwd(const LhShape& s, const void* qs, const void* ks, 
   auto q = (const float*)qs;
   auto k = (const float*)ks;
   auto v = (const float*)vs;
-  if (s.D == 128) hipLaunchKernelGGL(sdpa_fwd_f32<128>, grid, dim3(RT), 0, st, q, k, v, (float*)os, lse, s.S, s.scale);
-  else hipLaunchKernelGGL(sdpa_fwd_f32<64>, grid, dim3(RT), 0, st, q, k, v, (float*)os, lse, s.S, s.scale);
+  if (s.D == 128)
+    hipLaunchKernelGGL(sdpa_fwd_f32<128>, grid, dim3(RT), 0, st, q, k, v, (float*)os, lse, s.S, s.scale, s.Hq, s.Hs, s.Gq);
+  else
+    hipLaunchKernelGGL(sdpa_fwd_f32<64>, grid, dim3(RT), 0, st, q, k, v, (float*)os, lse, s.S, s.scale, s.Hq, s.Hs, s.Gq);
   return hipGetLastError();
 }
 
@@ -251,13 +260,18 @@ hipError_t lh_launch_sdpa_bwd(const LhShape& s, const void* qs, const void* ks, 
   auto k = (const float*)ks;
   auto v = (const float*)vs;
   auto g = (const float*)dos;
-  dim3 gk((unsigned)((s.S + RT - 1) / RT), (unsigned)BH);
+  dim3 gq((unsigned)((s.S + RT - 1) / RT), (unsigned)BH);
+  dim3 gk((unsigned)((s.S + RT - 1) / RT), (unsigned)(s.B * s.Hs));  // per selection head
   if (s.D == 128) {
-    hipLaunchKernelGGL(sdpa_bwd_dkdv_f32<128>, gk, dim3(RT), 0, st, q, k, v, g, lse, delta, (float*)dks, (float*)dvs, s.S, s.scale);
-    hipLaunchKernelGGL(sdpa_bwd_dq_f32<128>, gk, dim3(RT), 0, st, q, k, v, g, lse, delta, (float*)dqs, s.S, s.scale);
+    hipLaunchKernelGGL(sdpa_bwd_dkdv_f32<128>, gk, dim3(RT), 0, st, q, k, v, g, lse, delta, (float*)dks, (float*)dvs,
+                       s.S, s.scale, s.Hq, s.Hs, s.Gq);
+    hipLaunchKernelGGL(sdpa_bwd_dq_f32<128>, gq, dim3(RT), 0, st, q, k, v, g, lse, delta, (float*)dqs, s.S, s.scale,
+                       s.Hq, s.Hs, s.Gq);
   } else {
-    hipLaunchKernelGGL(sdpa_bwd_dkdv_f32<64>, gk, dim3(RT), 0, st, q, k, v, g, lse, delta, (float*)dks, (float*)dvs, s.S, s.scale);
-    hipLaunchKernelGGL(sdpa_bwd_dq_f32<64>, gk, dim3(RT), 0, st, q, k, v, g, lse, delta, (float*)dqs, s.S, s.scale);
+    hipLaunchKernelGGL(sdpa_bwd_dkdv_f32<64>, gk, dim3(RT), 0, st, q, k, v, g, lse, delta, (float*)dks, (float*)dvs,
+                       s.S, s.scale, s.Hq, s.Hs, s.Gq);
+    hipLaunchKernelGGL(sdpa_bwd_dq_f32<64>, gq, dim3(RT), 0, st, q, k, v, g, lse, delta, (float*)dqs, s.S, s.scale,
+                       s.Hq, s.Hs, s.Gq);
   }
   return hipGetLastError();
 }

@@ -59,6 +59,9 @@
 #ifndef LH_CQ
 #define LH_CQ 64  // dK/dV: query rows per tile
 #endif
+#ifndef LH_ORDER
+#define LH_ORDER 1  // 1: blocks ordered by work across all heads (longest first); 0: head by head
+#endif
 #ifndef LH_FNS
 #define LH_FNS 2  // forward: tile slots in the LDS ring
 #endif
@@ -214,6 +217,30 @@ struct SdpaIdx {
   int32_t Hq, Hkv, G;
 };
 
+// Query heads and selection heads: query head hq reads the gathered K~, V~ (and idx) of
+// selection head hq / Gq; there are Hs selection heads per batch (Hs = Hq, Gq = 1 when every
+// query head selects on its own).
+struct HeadMap {
+  int32_t Hq, Hs, Gq;
+};
+
+// Block order. Blocks are dispatched in linear-id order and go round-robin to the 8 XCDs. With
+// LH_ORDER = 1 linear id = rank * heads + head, where rank 0 is the longest block of a head
+// (most causal tiles): the longest blocks of every head start first, so no long block is left
+// to run alone at the end, and (heads being a multiple of 8) every block of a head lands on the
+// same XCD, whose L2 then holds that head's streamed tiles.
+struct BlockPos {
+  int rank;      // 0 = the head's longest block
+  int64_t head;  // blockIdx.y of the head-by-head order
+};
+__device__ __forceinline__ BlockPos block_pos() {
+  if (LH_ORDER) {
+    const int64_t lin = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+    return BlockPos{(int)(lin / gridDim.y), lin % gridDim.y};
+  }
+  return BlockPos{(int)blockIdx.x, (int64_t)blockIdx.y};
+}
+
 struct RowSrc {
   const bf16_t* l0;  // row 0 of the head in the input
   const bf16_t* py;  // row 0 of the head in the pyramid
@@ -340,7 +367,7 @@ constexpr int FW = LH_FW, FQ = 32 * LH_FW, FK = LH_FK, FNS = LH_FNS;
 template <int D, bool IDX>
 __global__ void __launch_bounds__(64 * FW) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
-              bf16_t* __restrict__ O, float* __restrict__ LSE, int S, float sl2, SdpaIdx ix) {
+              bf16_t* __restrict__ O, float* __restrict__ LSE, int S, float sl2, SdpaIdx ix, HeadMap hm) {
   constexpr int RB = 2 * D;
   constexpr int NB = FK / 32;  // 32-key blocks per tile
   constexpr int LPT = 2 * loads_per_wave<D, FK, FW>();
@@ -349,14 +376,16 @@ sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const 
   LH_RING(bf16_t, Vs, FK * D);
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, r32 = lane & 31;
-  const int64_t bh = blockIdx.y;
+  const BlockPos bp = block_pos();
+  const int64_t bh = bp.head;
   const int nqt = (S + FQ - 1) / FQ;
-  const int q0 = (nqt - 1 - (int)blockIdx.x) * FQ;  // longest rows first
+  const int q0 = (nqt - 1 - bp.rank) * FQ;  // longest rows first
   const int qw = q0 + 32 * w;
   const int myq = qw + r32;
+  const int64_t kvh = (bh / hm.Hq) * hm.Hs + (bh % hm.Hq) / hm.Gq;  // selection head
   const bf16_t* Qh = Q + bh * S * D;
-  const bf16_t* Kh = K + bh * S * D;
-  const bf16_t* Vh = V + bh * S * D;
+  const bf16_t* Kh = K + kvh * S * D;
+  const bf16_t* Vh = V + kvh * S * D;
   const LaneOff<D> lo = lane_offsets<D, LH_SWZ_F>(lane);
   constexpr int LPW = loads_per_wave<D, FK, FW>();
   RowSrc qsrc{}, ksrc{}, vsrc{};
@@ -368,7 +397,7 @@ sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const 
     qsrc = row_src(ix.q, ix.qp, b, hq, ix.Hq, ix, D);
     ksrc = row_src(ix.k, ix.kp, b, g, ix.Hkv, ix, D);
     vsrc = row_src(ix.v, ix.vp, b, g, ix.Hkv, ix, D);
-    idxh = ix.idx + bh * S;
+    idxh = ix.idx + kvh * S;
   }
   auto load_kv = [&](int slot_, int r0) __attribute__((always_inline)) {
     bf16_t* kt_ = slot_ == 0 ? Ks[0] : slot_ == 1 ? Ks[1] : slot_ == 2 ? Ks[2] : Ks[3];
@@ -470,7 +499,7 @@ template <int D, bool IDX>
 __global__ void __launch_bounds__(64 * QW) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
                  const bf16_t* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ DELTA,
-                 bf16_t* __restrict__ dQ, int S, float sl2, float scale, SdpaIdx ix) {
+                 bf16_t* __restrict__ dQ, int S, float sl2, float scale, SdpaIdx ix, HeadMap hm) {
   constexpr int RB = 2 * D;
   constexpr int LPT = 2 * loads_per_wave<D, BK, QW>();
   static_assert(QNS >= 2 && QNS <= 4, "ring of 2 to 4 slots");
@@ -478,14 +507,16 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
   LH_RING(bf16_t, Vs, BK * D);
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, r32 = lane & 31;
-  const int64_t bh = blockIdx.y;
+  const BlockPos bp = block_pos();
+  const int64_t bh = bp.head;
   const int nqt = (S + BQ - 1) / BQ;
-  const int q0 = (nqt - 1 - (int)blockIdx.x) * BQ;
+  const int q0 = (nqt - 1 - bp.rank) * BQ;
   const int qw = q0 + 32 * w;
   const int myq = qw + r32;
+  const int64_t kvh = (bh / hm.Hq) * hm.Hs + (bh % hm.Hq) / hm.Gq;  // selection head
   const bf16_t* Qh = Q + bh * S * D;
-  const bf16_t* Kh = K + bh * S * D;
-  const bf16_t* Vh = V + bh * S * D;
+  const bf16_t* Kh = K + kvh * S * D;
+  const bf16_t* Vh = V + kvh * S * D;
   const bf16_t* dOh = dO + bh * S * D;
   const LaneOff<D> lo = lane_offsets<D, LH_SWZ_Q>(lane);
   constexpr int LPW = loads_per_wave<D, BK, QW>();
@@ -498,7 +529,7 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
     qsrc = row_src(ix.q, ix.qp, b, hq, ix.Hq, ix, D);
     ksrc = row_src(ix.k, ix.kp, b, g, ix.Hkv, ix, D);
     vsrc = row_src(ix.v, ix.vp, b, g, ix.Hkv, ix, D);
-    idxh = ix.idx + bh * S;
+    idxh = ix.idx + kvh * S;
     tile_ids<D, BK, QW>(idxh, 0, S, w, lane, kv_ids);
   }
   auto load_kv = [&](int slot_, int r0) __attribute__((always_inline)) {
@@ -589,11 +620,14 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
 constexpr int KWV = LH_KWV, CK = 32 * LH_KWV, CQ = LH_CQ;
 static_assert(CQ % 32 == 0 && CQ <= 64, "query tile of 32 or 64 rows");
 
-template <int D, bool IDX>
+// GRP: the workgroup's keys belong to a selection shared by hm.Gq query heads; their dK, dV sum
+// over those heads (one pass of the query-tile loop per head, the accumulators kept).
+template <int D, bool IDX, bool GRP>
 __global__ void __launch_bounds__(64 * KWV) __attribute__((amdgpu_waves_per_eu(LH_KWV_EU, LH_KWV_EU)))
 sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
                    const bf16_t* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ DELTA,
-                   bf16_t* __restrict__ dK, bf16_t* __restrict__ dV, int S, float sl2, float scale, SdpaIdx ix) {
+                   bf16_t* __restrict__ dK, bf16_t* __restrict__ dV, int S, float sl2, float scale, SdpaIdx ix,
+                   HeadMap hm) {
   constexpr int RB = 2 * D;
   // LDS is laid out by decreasing alignment: the lse / Delta rows (1 KB) first, then the query
   // tiles, so that both sit inside the first 64 KB, where a base address folds into the 16-bit
@@ -603,13 +637,17 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
   __shared__ __align__(16) bf16_t Kw[CK * D];
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, r32 = lane & 31;
-  const int64_t bh = blockIdx.y;
-  const int k0 = (int)blockIdx.x * CK;  // early keys see the most queries: launched first
+  const BlockPos bp = block_pos();
+  const int64_t bs = bp.head;  // b * Hs + hs: the selection head whose keys this block owns
+  const int64_t bsb = bs / hm.Hs;
+  const int hs0 = (int)(bs - bsb * hm.Hs);
+  int64_t bh = bsb * hm.Hq + (int64_t)hs0 * hm.Gq;  // the query head being streamed
+  const int k0 = bp.rank * CK;  // early keys see the most queries: launched first
   const int kw = k0 + 32 * w;
   const int mykey = kw + r32;
   const bf16_t* Qh = Q + bh * S * D;
-  const bf16_t* Kh = K + bh * S * D;
-  const bf16_t* Vh = V + bh * S * D;
+  const bf16_t* Kh = K + bs * S * D;
+  const bf16_t* Vh = V + bs * S * D;
   const bf16_t* dOh = dO + bh * S * D;
   const float* Lh = LSE + bh * S;
   const float* Dh = DELTA + bh * S;
@@ -618,12 +656,11 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
   const int32_t* idxh = nullptr;
   int32_t q_ids[loads_per_wave<D, CQ, KWV>()];  // ids of the next query tile to be staged
   if constexpr (IDX) {
-    const int64_t b = bh / ix.Hq;
-    const int hq = (int)(bh - b * ix.Hq), g = hq / ix.G;
-    qsrc = row_src(ix.q, ix.qp, b, hq, ix.Hq, ix, D);
-    ksrc = row_src(ix.k, ix.kp, b, g, ix.Hkv, ix, D);
-    vsrc = row_src(ix.v, ix.vp, b, g, ix.Hkv, ix, D);
-    idxh = ix.idx + bh * S;
+    const int hq = hs0 * hm.Gq, g = hq / ix.G;
+    qsrc = row_src(ix.q, ix.qp, bsb, hq, ix.Hq, ix, D);
+    ksrc = row_src(ix.k, ix.kp, bsb, g, ix.Hkv, ix, D);
+    vsrc = row_src(ix.v, ix.vp, bsb, g, ix.Hkv, ix, D);
+    idxh = ix.idx + bs * S;
   }
 
   const int qstart = (k0 / CQ) * CQ;
@@ -728,8 +765,24 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
   const int nfree = nqt > CK / CQ ? nqt - CK / CQ : 0;
   auto plain = [&](auto bufc, int it) __attribute__((always_inline)) { tile(bufc, IC<0>{}, it); };
   auto masked = [&](auto bufc, int it) __attribute__((always_inline)) { tile(bufc, IC<1>{}, it); };
-  ring2_loop(0, nfree, plain);
-  ring2_loop(nfree, nqt, masked);
+  for (int mq = 0;;) {
+    ring2_loop(0, nfree, plain);
+    ring2_loop(nfree, nqt, masked);
+    if (!GRP || ++mq >= hm.Gq) break;
+    // next query head of the selection: restart the tile stream once every wave is done with
+    // the buffers of the last tile
+    __syncthreads();
+    ++bh;
+    Qh += (int64_t)S * D;
+    dOh += (int64_t)S * D;
+    Lh += S;
+    Dh += S;
+    if constexpr (IDX) {
+      qsrc = row_src(ix.q, ix.qp, bsb, hs0 * hm.Gq + mq, ix.Hq, ix, D);
+      tile_ids<D, CQ, KWV>(idxh, qlast, S, w, lane, q_ids);
+    }
+    stage(IC<0>{}, qlast);
+  }
   // C layout: row = key kw + 8(i/4) + 4h + i%4, column 32 d + lane % 32
 #pragma unroll
   for (int d = 0; d < D / 32; ++d)
@@ -737,8 +790,8 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
     for (int i = 0; i < 16; ++i) {
       const int key = kw + 8 * (i >> 2) + 4 * h + (i & 3);
       if (key < S) {
-        dK[(bh * S + key) * D + 32 * d + r32] = f2bf(dkacc[d][i] * scale);
-        dV[(bh * S + key) * D + 32 * d + r32] = f2bf(dvacc[d][i]);
+        dK[(bs * S + key) * D + 32 * d + r32] = f2bf(dkacc[d][i] * scale);
+        dV[(bs * S + key) * D + 32 * d + r32] = f2bf(dvacc[d][i]);
       }
     }
 }
@@ -747,40 +800,49 @@ template <bool IDX>
 static void launch_fwd(const LhShape& s, const void* qs, const void* ks, const void* vs, void* os, float* lse,
                        const SdpaIdx& ix, hipStream_t st) {
   const int S = (int)s.S;
+  const HeadMap hm{s.Hq, s.Hs, s.Gq};
   dim3 grid((unsigned)((S + FQ - 1) / FQ), (unsigned)(s.B * s.Hq));
   const float sl2 = s.scale * kLog2e;
   auto q = (const bf16_t*)qs;
   auto k = (const bf16_t*)ks;
   auto v = (const bf16_t*)vs;
   if (s.D == 128)
-    hipLaunchKernelGGL((sdpa_fwd_bf16<128, IDX>), grid, dim3(64 * FW), 0, st, q, k, v, (bf16_t*)os, lse, S, sl2, ix);
+    hipLaunchKernelGGL((sdpa_fwd_bf16<128, IDX>), grid, dim3(64 * FW), 0, st, q, k, v, (bf16_t*)os, lse, S, sl2, ix,
+                       hm);
   else
-    hipLaunchKernelGGL((sdpa_fwd_bf16<64, IDX>), grid, dim3(64 * FW), 0, st, q, k, v, (bf16_t*)os, lse, S, sl2, ix);
+    hipLaunchKernelGGL((sdpa_fwd_bf16<64, IDX>), grid, dim3(64 * FW), 0, st, q, k, v, (bf16_t*)os, lse, S, sl2, ix, hm);
+}
+
+template <int D, bool IDX, bool GRP>
+static void launch_bwd_D(const LhShape& s, const bf16_t* q, const bf16_t* k, const bf16_t* v, const bf16_t* g,
+                         const float* lse, const float* delta, void* dqs, void* dks, void* dvs, const SdpaIdx& ix,
+                         hipStream_t st) {
+  const int S = (int)s.S;
+  const float sl2 = s.scale * kLog2e;
+  const HeadMap hm{s.Hq, s.Hs, s.Gq};
+  dim3 gk((unsigned)((S + CK - 1) / CK), (unsigned)(s.B * s.Hs));  // per (key block, selection head)
+  dim3 gq((unsigned)((S + BQ - 1) / BQ), (unsigned)(s.B * s.Hq));
+  hipLaunchKernelGGL((sdpa_bwd_dkdv_bf16<D, IDX, GRP>), gk, dim3(64 * KWV), 0, st, q, k, v, g, lse, delta,
+                     (bf16_t*)dks, (bf16_t*)dvs, S, sl2, s.scale, ix, hm);
+  hipLaunchKernelGGL((sdpa_bwd_dq_bf16<D, IDX>), gq, dim3(64 * QW), 0, st, q, k, v, g, lse, delta, (bf16_t*)dqs, S,
+                     sl2, s.scale, ix, hm);
 }
 
 template <bool IDX>
 static void launch_bwd(const LhShape& s, const void* qs, const void* ks, const void* vs, const void* dos,
                        const float* lse, const float* delta, void* dqs, void* dks, void* dvs, const SdpaIdx& ix,
                        hipStream_t st) {
-  const int S = (int)s.S;
-  const int64_t BH = s.B * s.Hq;
-  const float sl2 = s.scale * kLog2e;
   auto q = (const bf16_t*)qs;
   auto k = (const bf16_t*)ks;
   auto v = (const bf16_t*)vs;
   auto g = (const bf16_t*)dos;
-  dim3 gk((unsigned)((S + CK - 1) / CK), (unsigned)BH);
-  dim3 gq((unsigned)((S + BQ - 1) / BQ), (unsigned)BH);
+  const bool grp = s.Gq > 1;
   if (s.D == 128) {
-    hipLaunchKernelGGL((sdpa_bwd_dkdv_bf16<128, IDX>), gk, dim3(64 * KWV), 0, st, q, k, v, g, lse, delta,
-                       (bf16_t*)dks, (bf16_t*)dvs, S, sl2, s.scale, ix);
-    hipLaunchKernelGGL((sdpa_bwd_dq_bf16<128, IDX>), gq, dim3(64 * QW), 0, st, q, k, v, g, lse, delta,
-                       (bf16_t*)dqs, S, sl2, s.scale, ix);
+    if (grp) launch_bwd_D<128, IDX, true>(s, q, k, v, g, lse, delta, dqs, dks, dvs, ix, st);
+    else launch_bwd_D<128, IDX, false>(s, q, k, v, g, lse, delta, dqs, dks, dvs, ix, st);
   } else {
-    hipLaunchKernelGGL((sdpa_bwd_dkdv_bf16<64, IDX>), gk, dim3(64 * KWV), 0, st, q, k, v, g, lse, delta,
-                       (bf16_t*)dks, (bf16_t*)dvs, S, sl2, s.scale, ix);
-    hipLaunchKernelGGL((sdpa_bwd_dq_bf16<64, IDX>), gq, dim3(64 * QW), 0, st, q, k, v, g, lse, delta,
-                       (bf16_t*)dqs, S, sl2, s.scale, ix);
+    if (grp) launch_bwd_D<64, IDX, true>(s, q, k, v, g, lse, delta, dqs, dks, dvs, ix, st);
+    else launch_bwd_D<64, IDX, false>(s, q, k, v, g, lse, delta, dqs, dks, dvs, ix, st);
   }
 }
 

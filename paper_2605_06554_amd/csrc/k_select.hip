@@ -31,6 +31,7 @@ struct SelArgs {
   int32_t* ws;  // [B, Hq, Scand] candidate lists, level-major
   int64_t Ptot, Scand;
   int32_t Hq, Hkv, G, L, p;
+  int32_t Hs, Gq;  // selection heads; query heads whose scores one selection ranks
   int64_t off[17];
   int64_t cand[16];
   int64_t npar[16];
@@ -69,13 +70,14 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
   __shared__ uint32_t sel_state[2];  // prefix, remaining
 
   const int tid = threadIdx.x;
-  const int bh = blockIdx.x;  // b * Hq + hq
-  const int hq = bh % a.Hq;
-  const int64_t b = bh / a.Hq;
-  const int g = hq / a.G;
-  const float* sq = a.s_qk + (int64_t)bh * a.Ptot;
+  const int bs = blockIdx.x;  // b * Hs + hs
+  const int hs = bs % a.Hs;
+  const int64_t b = bs / a.Hs;
+  const int g = hs * a.Gq / a.G;  // KV head
+  // query score rows of the selection: query heads hs Gq .. hs Gq + Gq - 1
+  const float* sq = a.s_qk + (b * a.Hq + (int64_t)hs * a.Gq) * a.Ptot;
   const float* sk = a.s_kq + (b * a.Hkv + g) * a.Ptot;
-  int32_t* C = a.ws + (int64_t)bh * a.Scand;
+  int32_t* C = a.ws + (int64_t)bs * a.Scand;
   const int L = a.L, p = a.p;
 
   // top level: every entry is a candidate
@@ -100,7 +102,12 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
     if (kk == 0) continue;
     for (int64_t u = tid; u < n; u += kSelThreads) {
       const int32_t i = Cl[u];
-      const float x = sql[i], y = skl[i];
+      float x = sql[i];
+      for (int t = 1; t < a.Gq; ++t) {  // the max over the query heads of a shared selection
+        const float z = sql[(int64_t)t * a.Ptot + i];
+        x = x > z ? x : z;
+      }
+      const float y = skl[i];
       keys[u] = __float_as_uint(x > y ? x : y);
     }
     __syncthreads();
@@ -253,7 +260,7 @@ using namespace lh;
 
 hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_kq, int32_t* idx,
                             int32_t* slot, int32_t* ws, hipStream_t st) {
-  const int64_t BH = s.B * s.Hq;
+  const int64_t BH = s.B * s.Hs;  // one selection per (b, selection head)
   // slot = -1 everywhere (a fill kernel, so the sequence can be captured in a graph)
   {
     const int64_t n = BH * s.Ptot;
@@ -271,6 +278,8 @@ hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_
   a.Hq = s.Hq;
   a.Hkv = s.Hkv;
   a.G = s.G;
+  a.Hs = s.Hs;
+  a.Gq = s.Gq;
   a.L = s.L;
   a.p = s.p;
   for (int l = 0; l < 17; ++l) a.off[l] = s.off[l], a.coff[l] = s.coff[l];

@@ -107,6 +107,8 @@ __device__ __forceinline__ void store_chunk<bf16_t>(bf16_t* p, const float* v) {
 struct LhShape {
   int64_t B, N;
   int32_t Hq, Hkv, D, p, L, k, G;  // G = Hq / Hkv
+  int32_t Hs, Gq;  // selection heads and query heads per selection head: (Hq, 1), or (Hkv, G)
+                   // with LH_FLAG_GQA_SHARED; query head hq uses selection head hq / Gq
   int32_t dtype;
   float scale;
   uint32_t flags;

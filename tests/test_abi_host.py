@@ -45,7 +45,7 @@ def _pr(**kw):
     (dict(Hq=3, Hkv=2), -3),
     (dict(D=96), -3),
     (dict(dtype=7), -4),
-    (dict(flags=4), -3),
+    (dict(flags=8), -3),
     (dict(N=0), -2),
     (dict(L=1, p=0), 0),                # p is irrelevant with one level
     (dict(N=2 ** 20, L=2, k=1000), -3),  # one level would rank 262144 candidates

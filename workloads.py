@@ -78,6 +78,10 @@ TEST_CONFIGS = {
     "t_l2": Config("t_l2", 1, 1028, 2, 2, 64, 4, 2, 64, "bf16", 2007),
     # p = 2, L = 5, N = 112: Ptot = 217 (odd), three query heads per KV head
     "t_g3": Config("t_g3", 1, 112, 3, 1, 64, 2, 5, 5, "bf16", 2008),
+    # one selection per KV group (flag bit 2): G = 2, p = 4; G = 3, p = 2; G = 4 in fp32
+    "t_gqs": Config("t_gqs", 1, 4096, 4, 2, 128, 4, 4, 256, "bf16", 2009, "spikes", 0.01, flags=4),
+    "t_gqs3": Config("t_gqs3", 1, 2048, 6, 2, 64, 2, 5, 40, "bf16", 2010, flags=4),
+    "t_gqs_f32": Config("t_gqs_f32", 1, 1024, 4, 1, 64, 4, 3, 64, "fp32", 2011, flags=4),
 }
 
 
