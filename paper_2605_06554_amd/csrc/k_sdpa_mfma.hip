@@ -102,7 +102,7 @@ using IC = std::integral_constant<int, N>;
 #define LH_SWZ_Q 2  // dQ
 #endif
 #ifndef LH_SWZ_K
-#define LH_SWZ_K 3  // dK/dV (its register budget has no room for the extra offsets)
+#define LH_SWZ_K 2  // dK/dV
 #endif
 template <int D, int SW>
 __device__ __forceinline__ int swz(int r) {
