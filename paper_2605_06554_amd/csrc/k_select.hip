@@ -1,13 +1,15 @@
 // k_select.hip -- hierarchical selection (Sec. 3.4, Eq. topk with Fig. 2 panel 3) and causal
 // ordering of the selected entries (Sec. 3.5, mask paragraph).
 //
-// select_kernel: one workgroup of 1024 threads per (b, hq). Per level l = L-1 .. 1 it ranks the
-// level's candidates (a sorted list of level-local indices) by the 32-bit key
+// select_kernel: one workgroup of 1024 threads per (b, selection head). Per level l = L-1 .. 1
+// it ranks the level's candidates (a sorted list of level-local indices) by the 32-bit key
 // bits(max(s_QK, s_KQ)) -- non-negative floats, so the bit pattern orders them -- and finds the
-// exact threshold of the k best by an MSB-first radix select (four 8-bit digits, LDS
-// histograms with integer atomics). A stable compaction in candidate order then takes every
-// key above the threshold and the first (lower-index) ties, and writes the p children of each
-// parent -- which are the next level's candidates, already sorted -- into the workspace.
+// exact threshold of the k best by an MSB-first radix select (8-bit digits below the bits all
+// keys share, LDS histograms with integer atomics; one wave reads each digit off the histogram
+// with a suffix scan). A stable compaction in candidate order then takes every key above the threshold and
+// the first (lower-index) ties, and writes the p children of each parent -- which are the next
+// level's candidates, already sorted -- into the workspace. In the compaction each wave walks
+// a contiguous range of candidates and ranks them with ballots.
 // With LH_FLAG_STRATIFIED (App. D.2) the same select and compaction run on every chunk of 2048
 // consecutive candidates, each keeping its proportional share of the k parents.
 // No floating-point atomics: the result is bitwise deterministic.
@@ -15,7 +17,8 @@
 // order_kernel: one thread per candidate. Emitted entries are sorted by
 // key = e * L + (L - 1 - l), e = (i + 1) p^l - 1 (window end, coarser level first on ties).
 // Each level's list is sorted by i, hence by key, so an entry's rank is the sum over levels of
-// a binary search (merge by rank, no general sort). It writes idx[rank] and slot[id] = rank.
+// a binary search (merge by rank, no general sort); the searches of the levels advance in
+// lockstep. It writes idx[rank] and slot[id] = rank.
 #include "lh_common.h"
 
 namespace lh {
@@ -39,37 +42,46 @@ struct SelArgs {
   int32_t stratified;  // LH_FLAG_STRATIFIED: per-chunk shares instead of one top-k per level
 };
 
-// Exclusive prefix sum over the 1024 threads of the block; returns the exclusive value and
-// writes the block total. `sh` holds kSelWaves ints.
-__device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int* total) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int inc = v;
+// One wave picks the digit of the quota-th largest key from the 256-bin histogram: the highest
+// bin whose count, added to the counts of every higher bin, reaches the remaining quota. The
+// remaining quota drops by the count of the higher bins. Lane l holds bins 4l .. 4l + 3; a
+// suffix sum over the lanes finds the one lane where the running count crosses the quota.
+__device__ __forceinline__ void select_bin(const int* hist, uint32_t* sel_state, uint32_t prefix, int shift,
+                                           int lane) {
+  const uint32_t rem = sel_state[1];
+  const int4 hb = *reinterpret_cast<const int4*>(hist + 4 * lane);
+  const uint32_t lsum = (uint32_t)(hb.x + hb.y + hb.z + hb.w);
+  uint32_t suf = lsum;  // counts of bins 4 lane .. 255
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
-    const int t = __shfl_up(inc, d, 64);
-    if (lane >= d) inc += t;
+    const uint32_t t = __shfl_down(suf, d, 64);
+    if (lane + d < 64) suf += t;
   }
-  if (lane == 63) sh[w] = inc;
-  __syncthreads();
-  int wsum = 0, tot = 0;
-#pragma unroll
-  for (int i = 0; i < kSelWaves; ++i) {
-    const int x = sh[i];
-    if (i < w) wsum += x;
-    tot += x;
+  const uint32_t above = suf - lsum;  // counts of bins 4 lane + 4 .. 255
+  const uint32_t c[4] = {(uint32_t)hb.x, (uint32_t)hb.y, (uint32_t)hb.z, (uint32_t)hb.w};
+  if (above < rem && above + lsum >= rem) {
+    uint32_t acc = above;
+    int j = 3;
+    for (; j > 0; --j) {
+      if (acc + c[j] >= rem) break;
+      acc += c[j];
+    }
+    sel_state[0] = prefix | ((uint32_t)(4 * lane + j) << shift);
+    sel_state[1] = rem - acc;
+  } else if (lane == 0 && suf < rem) {  // fewer keys than the quota (not reached): bin 0
+    sel_state[0] = prefix;
+    sel_state[1] = rem - (suf - c[0]);
   }
-  __syncthreads();
-  *total = tot;
-  return wsum + inc - v;
 }
 
 __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
   extern __shared__ uint32_t keys[];  // candidate keys of the current level
-  __shared__ int hist[256];
-  __shared__ int scan_sh[kSelWaves];
+  __shared__ __align__(16) int hist[256];
   __shared__ uint32_t sel_state[2];  // prefix, remaining
+  __shared__ int wave_cnt[kSelWaves];  // (greater << 16) | equal counts of each wave's candidates
+  __shared__ uint32_t key_and[kSelWaves], key_or[kSelWaves];  // per-wave AND / OR of the keys
 
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int bs = blockIdx.x;  // b * Hs + hs
   const int hs = bs % a.Hs;
   const int64_t b = bs / a.Hs;
@@ -100,15 +112,34 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
       continue;
     }
     if (kk == 0) continue;
-    for (int64_t u = tid; u < n; u += kSelThreads) {
-      const int32_t i = Cl[u];
-      float x = sql[i];
-      for (int t = 1; t < a.Gq; ++t) {  // the max over the query heads of a shared selection
-        const float z = sql[(int64_t)t * a.Ptot + i];
-        x = x > z ? x : z;
+    // keys of the level, kB candidates per thread at a time: the id loads, then the score
+    // loads, are each in flight together
+    constexpr int kB = 8;
+    for (int64_t u0 = tid; u0 < n; u0 += (int64_t)kSelThreads * kB) {
+      int32_t ids[kB];
+      float x[kB], y[kB];
+#pragma unroll
+      for (int j = 0; j < kB; ++j) {
+        const int64_t u = u0 + (int64_t)j * kSelThreads;
+        ids[j] = u < n ? Cl[u] : 0;
       }
-      const float y = skl[i];
-      keys[u] = __float_as_uint(x > y ? x : y);
+#pragma unroll
+      for (int j = 0; j < kB; ++j) {
+        x[j] = sql[ids[j]];
+        y[j] = skl[ids[j]];
+      }
+      for (int t = 1; t < a.Gq; ++t) {  // the max over the query heads of a shared selection
+#pragma unroll
+        for (int j = 0; j < kB; ++j) {
+          const float z = sql[(int64_t)t * a.Ptot + ids[j]];
+          x[j] = x[j] > z ? x[j] : z;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kB; ++j) {
+        const int64_t u = u0 + (int64_t)j * kSelThreads;
+        if (u < n) keys[u] = __float_as_uint(x[j] > y[j] ? x[j] : y[j]);
+      }
     }
     __syncthreads();
     // One chunk covers the whole level in the exact mode. In the stratified mode chunk [s0, e0)
@@ -120,57 +151,105 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
       const int64_t first = a.stratified ? (kk * s0) / n : 0;
       const int64_t quota = a.stratified ? (kk * e0) / n - first : kk;
       if (quota == 0) continue;
+      // The bits every key of the chunk shares need no radix pass: a block AND / OR of the keys
+      // gives them, and the digits start at the highest bit that varies.
+      uint32_t kand = 0xffffffffu, kor = 0u;
+      for (int64_t u = s0 + tid; u < e0; u += kSelThreads) {
+        const uint32_t key = keys[u];
+        kand &= key;
+        kor |= key;
+      }
+#pragma unroll
+      for (int d = 32; d >= 1; d >>= 1) {
+        kand &= __shfl_xor(kand, d, 64);
+        kor |= __shfl_xor(kor, d, 64);
+      }
+      if (lane == 0) {
+        key_and[wv] = kand;
+        key_or[wv] = kor;
+      }
+      __syncthreads();
+      kand = 0xffffffffu;
+      kor = 0u;
+      for (int i = 0; i < kSelWaves; ++i) {
+        kand &= key_and[i];
+        kor |= key_or[i];
+      }
+      const int nb = (kand ^ kor) ? 32 - __clz(kand ^ kor) : 0;  // low bits that vary
       if (tid == 0) {
-        sel_state[0] = 0u;
+        sel_state[0] = nb == 32 ? 0u : (kor & ~((1u << nb) - 1u));
         sel_state[1] = (uint32_t)quota;
       }
       __syncthreads();
-      // MSB-first radix select of the quota-th largest key of the chunk
-      for (int shift = 24; shift >= 0; shift -= 8) {
+      // MSB-first radix select of the quota-th largest key of the chunk, 8 bits a pass
+      for (int hi = nb; hi > 0; hi -= 8) {
+        const int shift = hi > 8 ? hi - 8 : 0;
         for (int t = tid; t < 256; t += kSelThreads) hist[t] = 0;
         __syncthreads();
         const uint32_t prefix = sel_state[0];
-        const uint32_t himask = shift == 24 ? 0u : (0xffffffffu << (shift + 8));
+        const uint32_t himask = hi == 32 ? 0u : (0xffffffffu << hi);
+        const uint32_t dmask = (1u << (hi - shift)) - 1u;
         for (int64_t u = s0 + tid; u < e0; u += kSelThreads) {
           const uint32_t key = keys[u];
-          if ((key & himask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+          if ((key & himask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1);
         }
         __syncthreads();
-        if (tid == 0) {
-          uint32_t rem = sel_state[1];
-          int bin = 255;
-          for (; bin > 0; --bin) {
-            const uint32_t c = (uint32_t)hist[bin];
-            if (c >= rem) break;
-            rem -= c;
-          }
-          sel_state[0] = prefix | ((uint32_t)bin << shift);
-          sel_state[1] = rem;
-        }
+        if (tid < 64) select_bin(hist, sel_state, prefix, shift, tid);
         __syncthreads();
       }
       const uint32_t T = sel_state[0];
       const int need = (int)sel_state[1];  // ties at T to take, lowest candidate positions first
-      // stable compaction in candidate order (rounds of 1024 consecutive candidates)
-      int gt_before = 0, eq_before = 0;
-      for (int64_t base = s0; base < e0; base += kSelThreads) {
-        const int64_t u = base + tid;
-        uint32_t key = 0;
-        if (u < e0) key = keys[u];
-        const int gt = (u < e0 && key > T) ? 1 : 0;
-        const int eq = (u < e0 && key == T) ? 1 : 0;
-        int tot;
-        const int packed = block_exclusive_scan((gt << 16) | eq, scan_sh, &tot);
-        const int gt_rank = gt_before + (packed >> 16);
-        const int eq_rank = eq_before + (packed & 0xffff);
-        const bool take = gt || (eq && eq_rank < need);
-        if (take) {
-          const int64_t pos = first + gt_rank + (eq_rank < need ? eq_rank : need);
-          const int32_t i = Cl[u];
+      // stable compaction in candidate order: wave w owns the candidates [c0, c1) and walks
+      // them 64 at a time; ranks come from ballots, and the waves before it give its offsets
+      const int64_t per = ((e0 - s0 + kSelWaves - 1) / kSelWaves + 63) / 64 * 64;
+      const int64_t c0 = s0 + per * wv < e0 ? s0 + per * wv : e0;
+      const int64_t c1 = c0 + per < e0 ? c0 + per : e0;
+      // counting pass: each key of the wave's range is replaced by its candidate id with the
+      // class in the top bits (bit 31: above T, bit 30: equal to T). Ids of levels >= 1 are
+      // below N / p < 2^30, as the host keeps the pyramid below 2^31 rows. The writing pass
+      // then makes no global reads. Ids are loaded kB chunks at a time, all in flight together.
+      int gt_w = 0, eq_w = 0;
+      for (int64_t b0 = c0; b0 < c1; b0 += 64 * kB) {
+        int32_t ids[kB];
+#pragma unroll
+        for (int j = 0; j < kB; ++j) {
+          const int64_t u = b0 + 64 * j + lane;
+          ids[j] = u < c1 ? Cl[u] : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < kB; ++j) {
+          const int64_t u = b0 + 64 * j + lane;
+          const uint32_t key = u < c1 ? keys[u] : 0u;
+          const bool gt = u < c1 && key > T, eq = u < c1 && key == T;
+          gt_w += __popcll(__ballot(gt));
+          eq_w += __popcll(__ballot(eq));
+          if (u < c1) keys[u] = (uint32_t)ids[j] | (gt ? 0x80000000u : 0u) | (eq ? 0x40000000u : 0u);
+        }
+      }
+      if (lane == 0) wave_cnt[wv] = (gt_w << 16) | eq_w;
+      __syncthreads();
+      int gt_rank = 0, eq_rank = 0;  // candidates of the earlier waves
+      for (int i = 0; i < wv; ++i) {
+        const int x = wave_cnt[i];
+        gt_rank += x >> 16;
+        eq_rank += x & 0xffff;
+      }
+      const uint64_t below = (1ull << lane) - 1ull;
+      for (int64_t base = c0; base < c1; base += 64) {
+        const int64_t u = base + lane;
+        const uint32_t e = u < c1 ? keys[u] : 0u;
+        const bool gt = e >> 31, eq = (e >> 30) & 1u;
+        const uint64_t bg = __ballot(gt);
+        const uint64_t be = __ballot(eq);
+        const int gr = gt_rank + __popcll(bg & below);
+        const int er = eq_rank + __popcll(be & below);
+        if (gt || (eq && er < need)) {
+          const int64_t pos = first + gr + (er < need ? er : need);
+          const int32_t i = (int32_t)(e & 0x3fffffffu);
           for (int r = 0; r < p; ++r) Cn[pos * p + r] = i * p + r;
         }
-        gt_before += tot >> 16;
-        eq_before += tot & 0xffff;
+        gt_rank += __popcll(bg);
+        eq_rank += __popcll(be);
       }
       __syncthreads();  // sel_state and hist are reused by the next chunk
     }
@@ -196,18 +275,6 @@ __device__ __forceinline__ int64_t order_key(int64_t i, int l, const OrdArgs& a)
   return ((i + 1) * a.pw[l] - 1) * a.L + (a.L - 1 - l);
 }
 
-// number of entries of the sorted list c[0, n) at level l whose key is below K
-__device__ __forceinline__ int64_t count_below(const int32_t* c, int64_t n, int l, int64_t K,
-                                               const OrdArgs& a) {
-  int64_t lo = 0, hi = n;
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) >> 1;
-    if (order_key(c[mid], l, a) < K) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
 // number of entries of the sorted int list c[0, n) below value x
 __device__ __forceinline__ int64_t lower_bound_val(const int32_t* c, int64_t n, int64_t x) {
   int64_t lo = 0, hi = n;
@@ -217,6 +284,37 @@ __device__ __forceinline__ int64_t lower_bound_val(const int32_t* c, int64_t n, 
     else hi = mid;
   }
   return lo;
+}
+
+constexpr int kMaxL = 8;  // levels a problem may have (the host rejects L > 8)
+
+// Lower bounds in the sorted lists C + coff[l], l < kMaxL: lo[l] ends as the number of entries
+// v of list l with below(l, v) true (below is monotone along each list). The lists advance
+// together: every step loads one probe of each list still open before comparing any.
+template <typename F>
+__device__ __forceinline__ void lockstep_search(int32_t* lo, int32_t* hi, const OrdArgs& a, F below) {
+  const int32_t* C = a.ws + (int64_t)blockIdx.y * a.Scand;
+  for (;;) {
+    int32_t v[kMaxL];
+    bool open = false;
+#pragma unroll
+    for (int l = 0; l < kMaxL; ++l) {
+      v[l] = 0;
+      if (lo[l] < hi[l]) {
+        v[l] = C[a.coff[l] + ((lo[l] + hi[l]) >> 1)];
+        open = true;
+      }
+    }
+    if (!__builtin_amdgcn_ballot_w64(open)) break;
+#pragma unroll
+    for (int l = 0; l < kMaxL; ++l) {
+      if (lo[l] < hi[l]) {
+        const int32_t mid = (lo[l] + hi[l]) >> 1;
+        if (below(l, v[l])) lo[l] = mid + 1;
+        else hi[l] = mid;
+      }
+    }
+  }
 }
 
 __global__ void __launch_bounds__(256) order_kernel(OrdArgs a) {
@@ -233,16 +331,39 @@ __global__ void __launch_bounds__(256) order_kernel(OrdArgs a) {
     if (c < a.cand[l - 1] && C[a.coff[l - 1] + c] == i * a.p) return;
   }
   const int64_t K = order_key(i, l, a);
+  // The binary searches of the L lists run in lockstep: each step issues one independent probe
+  // per list, so a thread waits for about log2(max list) loads instead of L times as many.
+  int32_t lo[kMaxL], hi[kMaxL];
+#pragma unroll
+  for (int l2 = 0; l2 < kMaxL; ++l2) {
+    lo[l2] = 0;
+    hi[l2] = l2 < a.L ? (int32_t)a.cand[l2] : 0;
+  }
+  lockstep_search(lo, hi, a, [&](int l2, int32_t v) { return order_key(v, l2, a) < K; });
   int64_t rank = 0;
-  for (int l2 = 0; l2 < a.L; ++l2) {
-    const int32_t* c2 = C + a.coff[l2];
-    const int64_t lb = count_below(c2, a.cand[l2], l2, K, a);
-    int64_t cnt = lb;
-    if (a.replace && l2 >= 1) {
-      const int64_t x = lb < a.cand[l2] ? (int64_t)c2[lb] : a.nrows[l2];
-      cnt -= lower_bound_val(C + a.coff[l2 - 1], a.cand[l2 - 1], x * a.p) / a.p;
+#pragma unroll
+  for (int l2 = 0; l2 < kMaxL; ++l2) rank += lo[l2];
+  if (a.replace) {
+    // a selected parent is replaced by its children: the children below K are counted at the
+    // finer level, so the parents below K (those whose first child is below K) are taken off
+    int32_t lo2[kMaxL], hi2[kMaxL];
+    int32_t bound[kMaxL + 1];  // first entry of list l2 at or after K (or the row count past the end)
+#pragma unroll
+    for (int l2 = 0; l2 <= kMaxL; ++l2) bound[l2] = 0;
+#pragma unroll
+    for (int l2 = 0; l2 < kMaxL; ++l2) {
+      lo2[l2] = hi2[l2] = 0;
+      if (l2 >= 1 && l2 < a.L) {
+        const int32_t* c2 = C + a.coff[l2];
+        bound[l2] = lo[l2] < a.cand[l2] ? c2[lo[l2]] : (int32_t)a.nrows[l2];
+        hi2[l2 - 1] = (int32_t)a.cand[l2 - 1];
+      }
     }
-    rank += cnt;
+    // lists l2 - 1 are searched for bound[l2] * p (slot l2 - 1 of lo2 / hi2)
+    lockstep_search(lo2, hi2, a, [&](int l2, int32_t v) { return (int64_t)v < (int64_t)bound[l2 + 1] * a.p; });
+#pragma unroll
+    for (int l2 = 0; l2 + 1 < kMaxL; ++l2)
+      if (l2 + 1 < a.L) rank -= lo2[l2] / a.p;
   }
   if (rank < 0 || rank >= a.S) return;  // cannot happen for lists written by select_kernel
   a.idx[bh * a.S + rank] = (int32_t)(a.off[l] + i);
