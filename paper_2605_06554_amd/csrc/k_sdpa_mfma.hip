@@ -19,14 +19,17 @@
 // LDS tiles: rows of D bf16 (2D bytes, no padding) with an XOR swizzle of 16-byte chunks
 // (chunk c of row r sits at position c ^ swz(r)), filled straight from global memory with
 // global_load_lds_dwordx4 (no staging registers), double-buffered so the next tile streams in
-// while the current one is used. The forward and dQ kernels use a swizzle under which both read
+// while the current one is used. All three kernels use a swizzle under which both read
 // patterns are bank-conflict free (measured with SQ_LDS_BANK_CONFLICT): 16 consecutive rows
 // reading one logical chunk (b128 operand reads) land on 16 different chunk positions, and the
 // 4 consecutive rows of a transposed read, each reading an aligned group of 4 chunks, land in 4
-// different groups. The dK/dV kernel, short of registers, uses a swizzle of r % 8 that keeps
-// the transposed reads conflict free and costs a 2-way conflict on its row reads. Every lane's
-// LDS offsets are computed once; tile bases are compile-time constants (the tile loop is
-// unrolled over the ring of slots).
+// different groups. Every lane's LDS offsets are computed once; tile bases are compile-time
+// constants (the tile loop is unrolled over the ring of slots).
+//
+// Occupancy: the forward runs 12 waves per workgroup, 3 per SIMD (at most 168 registers), so
+// that two waves can be in their softmax while a third feeds the MFMA unit. The two backward
+// kernels hold 128 (dK/dV) or 160 (dQ) accumulator and operand registers per lane and run 2
+// waves per SIMD.
 //
 // Pipeline: each kernel keeps an NS-slot ring of tiles in LDS. Before using tile t, a wave
 // waits until at most (NS - 2) tiles' worth of its own LDS-DMA loads are outstanding (vmcnt
@@ -39,7 +42,10 @@
 #include "lh_common.h"
 
 #ifndef LH_FW
-#define LH_FW 8  // forward: waves per workgroup (32 query rows each)
+#define LH_FW 12  // forward: waves per workgroup (32 query rows each)
+#endif
+#ifndef LH_FEU
+#define LH_FEU 3  // forward: waves per SIMD the register budget targets
 #endif
 #ifndef LH_FK
 #define LH_FK 64  // forward: keys per tile
@@ -187,13 +193,10 @@ __device__ __forceinline__ void load_tile_rows(bf16_t* tile, const bf16_t* src, 
     const int pos = blk * 64 + lane;
     const int r = pos / CPR;
     const int c = (pos % CPR) ^ swz<D, SW>(r);
-    const char* g;
-    if constexpr (CLAMP) {
-      const int gr = r0 + r < S ? r0 + r : S - 1;
-      g = reinterpret_cast<const char*>(src + (int64_t)gr * D + c * 8);
-    } else {
-      g = base + (uint32_t)((r * D + c * 8) * 2);
-    }
+    // rows past S read row S - 1; the clamp stays a 32-bit lane offset from the tile's uniform
+    // base, so no lane holds a 64-bit address (fewer live registers in every kernel)
+    const int rr = CLAMP ? (r < S - 1 - r0 ? r : S - 1 - r0) : r;
+    const char* g = base + (int32_t)((rr * D + c * 8) * 2);
     __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
                                      (__attribute__((address_space(3))) void*)(tile + blk * 512), 16, 0, 0);
   }
@@ -365,7 +368,7 @@ constexpr int FW = LH_FW, FQ = 32 * LH_FW, FK = LH_FK, FNS = LH_FNS;
 
 // IDX: Q, K, V are unused; rows come from the input / pyramid through ix.idx.
 template <int D, bool IDX>
-__global__ void __launch_bounds__(64 * FW) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ void __launch_bounds__(64 * FW) __attribute__((amdgpu_waves_per_eu(LH_FEU, LH_FEU)))
 sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
               bf16_t* __restrict__ O, float* __restrict__ LSE, int S, float sl2, SdpaIdx ix, HeadMap hm) {
   constexpr int RB = 2 * D;
@@ -467,19 +470,42 @@ sdpa_fwd_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const 
         for (int i = 0; i < 16; ++i) oacc[d][i] *= alpha;
       m_run = mloc;
     }
-#pragma unroll
-    for (int st = 0; st < FK / 16; ++st) {
+    // P of 16 keys at a time. Step st + 1's softmax (independent of step st's MFMAs) is
+    // scheduled between step st's four P V MFMAs, each MFMA's V operand read one MFMA ahead.
+    float la = 0.0f, lb = 0.0f;
+    auto soft = [&](int st) __attribute__((always_inline)) {
       float f[8];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        f[t] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[st >> 1][8 * (st & 1) + t], sl2, -m_run));
-        l_run += f[t];
-      }
-      const bf16x8 pb = cvt8(f);
+      for (int t = 0; t < 8; ++t) f[t] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[st >> 1][8 * (st & 1) + t], sl2, -m_run));
+      la += (f[0] + f[1]) + (f[2] + f[3]);
+      lb += (f[4] + f[5]) + (f[6] + f[7]);
+      return cvt8(f);
+    };
+    bf16x8 pcur = soft(0);
+    asm volatile("" ::"v"(la), "v"(lb));  // the first step's sums stay ahead of the interleaving
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int st = 0; st < FK / 16; ++st) {
+      bf16x8 pnext = pcur;
+      if (st + 1 < FK / 16) pnext = soft(st + 1);
 #pragma unroll
       for (int d = 0; d < D / 32; ++d)
-        oacc[d] = mfma32(tr8(Vt, 16 * st * RB + lo.trl[d], 16 * st * RB + lo.trh[d]), pb, oacc[d]);
+        oacc[d] = mfma32(tr8(Vt, 16 * st * RB + lo.trl[d], 16 * st * RB + lo.trh[d]), pcur, oacc[d]);
+      if (st + 1 < FK / 16) {
+        // groups: DS reads (mask 0x100), MFMA (0x008), VALU (0x002), transcendental (0x400)
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+        for (int d = 0; d < D / 32; ++d) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          if (d + 1 < D / 32) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+          __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      pcur = pnext;
     }
+    l_run += la + lb;
   };
   for (int t0 = 0; t0 < nkt; t0 += FNS) SlotLoop<0, FNS>::run(t0, nkt, step);
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
