@@ -129,6 +129,39 @@ def test_select_random_scores(N, p, L, k, flags, ties, rng):
             check_equal(f"slot[{b},{hq}]", slot[b, hq], rs)
 
 
+@pytest.mark.parametrize("kind", ["constant", "low_bits", "wide", "zeros"])
+@pytest.mark.parametrize("N,p,L,k,flags", [(16384, 4, 5, 4096, 0), (65536, 4, 3, 8192, 2), (4096, 4, 4, 100, 1)])
+def test_select_key_bit_patterns(kind, N, p, L, k, flags, rng):
+    # Score patterns that drive the radix select's digit choice to its edges: every key equal
+    # (no digit pass at all), keys that differ only in the lowest mantissa bits (one short
+    # final digit), keys spanning many binades (a first digit at the sign/exponent byte),
+    # and mostly-zero scores with a few positive ones.
+    Hq, Hkv = 4, 2
+    print(f"[stage select bits] kind={kind} N={N} p={p} L={L} k={k} flags={flags}", flush=True)
+    pr = lh.problem(2, N, Hq, Hkv, 64, p, L, k, lh.LH_F32, 0.0, flags)
+    Ptot = lh.lh_pyramid_rows(pr)
+    shape_q, shape_k = (2, Hq, Ptot), (2, Hkv, Ptot)
+    if kind == "constant":
+        sq, sk = np.full(shape_q, 3.25, np.float32), np.full(shape_k, 3.25, np.float32)
+    elif kind == "low_bits":
+        base = np.uint32(np.float32(1.5).view(np.uint32))
+        sq = (base + rng.integers(0, 8, shape_q).astype(np.uint32)).view(np.float32)
+        sk = (base + rng.integers(0, 8, shape_k).astype(np.uint32)).view(np.float32)
+    elif kind == "wide":
+        sq = (2.0 ** rng.uniform(-60, 60, shape_q)).astype(np.float32)
+        sk = (2.0 ** rng.uniform(-60, 60, shape_k)).astype(np.float32)
+    else:
+        sq = np.where(rng.random(shape_q) < 0.01, rng.random(shape_q), 0.0).astype(np.float32)
+        sk = np.zeros(shape_k, np.float32)
+    idx, slot = _run_select(pr, torch.from_numpy(sq).to(DEV), torch.from_numpy(sk).to(DEV))
+    h = oracle.Head(N, 64, p, L, k, oracle.F32, flags)
+    for b in range(2):
+        for hq in range(Hq):
+            ri, rs = oracle.select(h, sq[b, hq], sk[b, hq // 2])
+            check_equal(f"idx[{b},{hq}]", idx[b, hq], ri)
+            check_equal(f"slot[{b},{hq}]", slot[b, hq], rs)
+
+
 def _layer_oracle(c, inp):
     q, k, v = (inp[x].double().numpy() for x in ("q", "k", "v"))
     return oracle.layer_forward(q, k, v, c.p, c.L, c.k, dtype=_odt(c), flags=c.flags)
