@@ -128,8 +128,9 @@ def run_gpu(args, cfg):
         lh.lh_attention_bwd(pr, idx, slot, qs, ks, vs, os_, lse, dout, dq, dk, dv, wsb, stream=stream)
 
     if args.traffic_probe:
-        # one forward (state for the backward), the adjoint of the scatter, then exactly one call
-        # of the SDPA backward, then a plain streaming kernel of known size for the counter scale
+        # one forward (state for the backward), the adjoint of the scatter, exactly one call of
+        # the SDPA backward, one of the gather+pool adjoint, then a plain streaming kernel of known
+        # size for the counter scale
         lh.lh_attention_fwd(pr, q, k, v, o, idx, slot, qs, ks, vs, os_, lse, wsf, stream=stream)
         dos1, dqs1 = (torch.empty(B, Hq, S, D, dtype=dt, device=dev) for _ in range(2))
         dks1, dvs1 = (torch.empty(B, Hs, S, D, dtype=dt, device=dev) for _ in range(2))
@@ -138,6 +139,10 @@ def run_gpu(args, cfg):
         torch.cuda.synchronize()
         print("[probe] sdpa_bwd call", file=sys.stderr, flush=True)
         lh.lh_sdpa_bwd(pr, qs, ks, vs, os_, lse, dos1, dqs1, dks1, dvs1, wsd1, stream=stream)
+        torch.cuda.synchronize()
+        print("[probe] gather_bwd call", file=sys.stderr, flush=True)
+        dq1, dk1, dv1 = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        lh.lh_gather_bwd(pr, dqs1, dks1, dvs1, slot, dq1, dk1, dv1, stream=stream)
         torch.cuda.synchronize()
         n = COPY_PROBE_BYTES // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
@@ -304,7 +309,7 @@ def main():
     ap.add_argument("--gqa-shared", action="store_true",
                     help="one selection per KV group (LH_FLAG_GQA_SHARED) instead of one per query head")
     ap.add_argument("--traffic-probe", action="store_true",
-                    help="run one SDPA backward call and one copy kernel (for rocprofv3 --pmc), then exit")
+                    help="run one layer forward, scatter adjoint, SDPA backward and gather adjoint, and one copy kernel (for rocprofv3 --pmc), then exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
