@@ -13,8 +13,9 @@
 //
 // Scores (Q and K only): rows are staged through LDS so that one thread computes one row's
 // squared norm sequentially (c ascending, fp64; 16-byte LDS reads), takes the correctly rounded
-// fp64 sqrt and rounds to fp32. One thread per head then max-pools the level-0 scores up the
-// levels.
+// fp64 sqrt and rounds to fp32. One thread per head slot (the block's last threads) max-pools
+// the level-0 scores up the levels, one step behind: a step's cascade runs while the next
+// step's norms are computed (two LDS score buffers).
 #include "lh_common.h"
 
 namespace lh {
@@ -62,6 +63,37 @@ __device__ __forceinline__ void store_mean(T* dst, const double* acc, double inv
   }
 }
 
+// Max-pool cascade of nrc level-0 scores (rows in order) of head slot g2 of the block: the
+// level-l window that a score completes is written, and its max carried one level up. The
+// running state (mx, scnt, sent) carries over between calls.
+template <int L, int LA>
+__device__ __forceinline__ void cascade_rows(const PoolArgs& a, const float* nrm, int nrc, int col, int g2,
+                                             int64_t b, float (&mx)[LA], int (&scnt)[LA + 1], int (&sent)[LA]) {
+  const int t2i = g2 < a.slot1 ? 0 : g2 < a.slot2 ? 1 : 2;
+  float* sb = a.t[t2i].s;
+  if (!sb) return;
+  const int h2 = g2 - (t2i == 0 ? 0 : t2i == 1 ? a.slot1 : a.slot2);
+  float* srow = sb + (b * a.t[t2i].H + h2) * a.Ptot;
+  for (int r = 0; r < nrc; ++r) {
+    const float s0 = nrm[r * a.HW + col];
+    mx[1] = mx[1] > s0 ? mx[1] : s0;
+    ++scnt[1];
+#pragma unroll
+    for (int l = 1; l < L; ++l) {
+      if (scnt[l] != a.p) break;
+      scnt[l] = 0;
+      srow[a.off[l] + (int64_t)blockIdx.x * a.epb[l] + sent[l]] = mx[l];
+      ++sent[l];
+      if (l + 1 < L) {
+        const int ln = l + 1 < L ? l + 1 : l;
+        mx[ln] = mx[ln] > mx[l] ? mx[ln] : mx[l];
+        ++scnt[ln];
+      }
+      mx[l] = 0.0f;
+    }
+  }
+}
+
 // PF > 0: p == PF is known at compile time and kPoolRB is a multiple of it, so level-1
 // windows close at fixed positions of every step. PF == 0: any p, checked row by row.
 template <typename T, int L, int PF>
@@ -90,12 +122,16 @@ __global__ void __launch_bounds__(256) pool_score_kernel(PoolArgs a) {
   const bool do_pool = L > 1 && active && pyr != nullptr;
   const bool any_score = a.t[0].s != nullptr || a.t[1].s != nullptr || a.t[2].s != nullptr;
 
-  // LDS: staged rows [RB][HW][D + pad] of T, then level-0 scores [RB][HW].
+  // LDS: staged rows [RB][HW][D + pad] of T, then two buffers of level-0 scores [RB][HW].
   // rows padded by 16 bytes: 16-byte aligned, and the norm threads (one row each, consecutive
   // rows) read 16-byte chunks without bank conflicts
   const int rowT = D + 16 / (int)sizeof(T);
   T* tile = reinterpret_cast<T*>(smem);
-  float* nrm = reinterpret_cast<float*>(smem + (size_t)kPoolRB * a.HW * rowT * sizeof(T));
+  float* nrm_buf = reinterpret_cast<float*>(smem + (size_t)kPoolRB * a.HW * rowT * sizeof(T));
+  // the cascade threads: the block's last HW threads, one per head slot
+  const int ct = tid - ((int)blockDim.x - a.HW);
+  const bool cthread = L > 1 && ct >= 0 && (int)blockIdx.y * a.HW + ct < a.nslots;
+  int step = 0, nr_prev = 0;
 
   const T* xrow = x + ((b * a.N + j0) * H + h) * D + cc * CH;
   const int64_t xstride = (int64_t)H * D;
@@ -114,7 +150,7 @@ __global__ void __launch_bounds__(256) pool_score_kernel(PoolArgs a) {
   int cnt[LA + 1];  // rows (level 1) or closed windows (level l > 1) in the open level-l window
 #pragma unroll
   for (int l = 0; l <= LA; ++l) cnt[l] = 0;
-  // cascade state of the score thread of this head slot
+  // cascade state (used by the cascade threads)
   float mx[LA];
 #pragma unroll
   for (int l = 0; l < LA; ++l) mx[l] = 0.0f;
@@ -192,7 +228,13 @@ __global__ void __launch_bounds__(256) pool_score_kernel(PoolArgs a) {
       }
     }
     if (any_score) {
+      float* nrm = nrm_buf + (step & 1) * kPoolRB * a.HW;
       __syncthreads();
+      // the previous step's cascade runs on the last threads while the first ones compute
+      // this step's norms
+      if (step > 0 && cthread)
+        cascade_rows<L, LA>(a, nrm_buf + ((step - 1) & 1) * kPoolRB * a.HW, nr_prev, ct,
+                            (int)blockIdx.y * a.HW + ct, b, mx, scnt, sent);
       // one thread per (row, head slot): sequential fp64 sum of squares, c ascending
       for (int e = tid; e < nr * a.HW; e += blockDim.x) {
         const int r = e / a.HW, hh = e - r * a.HW;
@@ -225,40 +267,16 @@ __global__ void __launch_bounds__(256) pool_score_kernel(PoolArgs a) {
         nrm[r * a.HW + hh] = sc;
         sb[(b * H2 + h2) * a.Ptot + j0 + rb + r] = sc;
       }
+      // this step's scores are complete and the previous cascade is done; `tile` may be
+      // rewritten, and the next step's cascade reads this step's score buffer
       __syncthreads();
-      // max-pool cascade: one thread per head slot, rows in order
-      if (L > 1 && tid < a.HW && blockIdx.y * a.HW + tid < a.nslots) {
-        const int g2 = blockIdx.y * a.HW + tid;
-        const int t2i = g2 < a.slot1 ? 0 : g2 < a.slot2 ? 1 : 2;
-        float* sb = t2i == 0 ? t0.s : t2i == 1 ? t1.s : t2.s;
-        if (sb) {
-          const int h2 = g2 - (t2i == 0 ? 0 : t2i == 1 ? a.slot1 : a.slot2);
-          const int H2 = t2i == 0 ? t0.H : t2i == 1 ? t1.H : t2.H;
-          float* srow = sb + (b * H2 + h2) * a.Ptot;
-          for (int r = 0; r < nr; ++r) {
-            const float s0 = nrm[r * a.HW + tid];
-            mx[1] = mx[1] > s0 ? mx[1] : s0;
-            ++scnt[1];
-#pragma unroll
-            for (int l = 1; l < L; ++l) {
-              if (scnt[l] != a.p) break;
-              scnt[l] = 0;
-              srow[a.off[l] + (int64_t)blockIdx.x * a.epb[l] + sent[l]] = mx[l];
-              ++sent[l];
-              if (l + 1 < L) {
-                const int ln = l + 1 < L ? l + 1 : l;
-                mx[ln] = mx[ln] > mx[l] ? mx[ln] : mx[l];
-                ++scnt[ln];
-              }
-              mx[l] = 0.0f;
-            }
-          }
-        }
-      }
-      // the next step rewrites `tile` only after every thread passed the barrier above, and
-      // `nrm` only after the next step's first barrier, which the cascade thread reaches last
+      nr_prev = nr;
     }
+    ++step;
   }
+  if (any_score && step > 0 && cthread)
+    cascade_rows<L, LA>(a, nrm_buf + ((step - 1) & 1) * kPoolRB * a.HW, nr_prev, ct, (int)blockIdx.y * a.HW + ct,
+                        b, mx, scnt, sent);
 }
 
 template <typename T, int L>
@@ -286,7 +304,7 @@ static hipError_t launch_T(const LhShape& s, PoolArgs& a, hipStream_t st) {
   dim3 block((unsigned)(a.HW * CPR));
   const bool score = a.t[0].s || a.t[1].s || a.t[2].s;
   const int rowT = s.D + 16 / (int)sizeof(T);
-  size_t shm = score ? (size_t)kPoolRB * a.HW * rowT * sizeof(T) + (size_t)kPoolRB * a.HW * sizeof(float) : 0;
+  size_t shm = score ? (size_t)kPoolRB * a.HW * rowT * sizeof(T) + 2 * (size_t)kPoolRB * a.HW * sizeof(float) : 0;
   switch (s.L) {
     case 1: launch_L<T, 1>(a, grid, block, shm, st); break;
     case 2: launch_L<T, 2>(a, grid, block, shm, st); break;
