@@ -76,6 +76,9 @@ TEST_CONFIGS = {
     "t_strat": Config("t_strat", 1, 16384, 2, 1, 64, 2, 3, 1500, "bf16", 2006, "spikes", 0.01, flags=2),
     # L = 2 with N = 4 * 257: the last run of p^2 positions is partial; Ptot = 1285 (odd)
     "t_l2": Config("t_l2", 1, 1028, 2, 2, 64, 4, 2, 64, "bf16", 2007),
+    # L = 2, N = 4 * 257, two query heads per KV head: the dK / dV gather adjoint sums a
+    # group over runs of 8 positions, and its last run is partial
+    "t_l2g": Config("t_l2g", 1, 1028, 4, 2, 64, 4, 2, 64, "bf16", 2012),
     # p = 2, L = 5, N = 112: Ptot = 217 (odd), three query heads per KV head
     "t_g3": Config("t_g3", 1, 112, 3, 1, 64, 2, 5, 5, "bf16", 2008),
     # one selection per KV group (flag bit 2): G = 2, p = 4; G = 3, p = 2; G = 4 in fp32
