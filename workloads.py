@@ -79,6 +79,10 @@ TEST_CONFIGS = {
     # L = 2, N = 4 * 257, two query heads per KV head: the dK / dV gather adjoint sums a
     # group over runs of 8 positions, and its last run is partial
     "t_l2g": Config("t_l2g", 1, 1028, 4, 2, 64, 4, 2, 64, "bf16", 2012),
+    # p = 3 and p = 5 with two query heads per KV head: the runs-of-p grouped adjoint (p = 3)
+    # and the generic scatter and adjoint kernels for p > 4
+    "t_p3g": Config("t_p3g", 1, 999, 4, 2, 64, 3, 3, 40, "bf16", 2013),
+    "t_p5g": Config("t_p5g", 1, 1000, 4, 2, 64, 5, 3, 30, "bf16", 2014),
     # p = 2, L = 5, N = 112: Ptot = 217 (odd), three query heads per KV head
     "t_g3": Config("t_g3", 1, 112, 3, 1, 64, 2, 5, 5, "bf16", 2008),
     # one selection per KV group (flag bit 2): G = 2, p = 4; G = 3, p = 2; G = 4 in fp32
