@@ -33,7 +33,7 @@ def _odt(c):
     return oracle.BF16 if c.dtype == "bf16" else oracle.F32
 
 
-STAGE_CFGS = ["c1", "t_gqa", "t_f32", "t_p3", "t_k0", "t_l2", "t_l2g", "t_p3g", "t_p5g", "t_g3"]
+STAGE_CFGS = ["c1", "t_gqa", "t_f32", "t_p3", "t_k0", "t_l2", "t_l2g", "t_p3g", "t_p5g", "t_l8", "t_g3"]
 
 
 @pytest.mark.parametrize("name", STAGE_CFGS + ["t_l1"])

@@ -83,6 +83,8 @@ TEST_CONFIGS = {
     # and the generic scatter and adjoint kernels for p > 4
     "t_p3g": Config("t_p3g", 1, 999, 4, 2, 64, 3, 3, 40, "bf16", 2013),
     "t_p5g": Config("t_p5g", 1, 1000, 4, 2, 64, 5, 3, 30, "bf16", 2014),
+    # L = 8, the deepest pyramid the kernels are instantiated for (p = 2, N = 2048)
+    "t_l8": Config("t_l8", 1, 2048, 2, 1, 64, 2, 8, 12, "bf16", 2015),
     # p = 2, L = 5, N = 112: Ptot = 217 (odd), three query heads per KV head
     "t_g3": Config("t_g3", 1, 112, 3, 1, 64, 2, 5, 5, "bf16", 2008),
     # one selection per KV group (flag bit 2): G = 2, p = 4; G = 3, p = 2; G = 4 in fp32
