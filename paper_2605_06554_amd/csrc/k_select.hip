@@ -286,19 +286,18 @@ __device__ __forceinline__ int64_t lower_bound_val(const int32_t* c, int64_t n, 
   return lo;
 }
 
-constexpr int kMaxL = 8;  // levels a problem may have (the host rejects L > 8)
 
-// Lower bounds in the sorted lists C + coff[l], l < kMaxL: lo[l] ends as the number of entries
-// v of list l with below(l, v) true (below is monotone along each list). The lists advance
+// Lower bounds in the sorted lists C + coff[l], l < NL: lo[l] ends as the number of entries v
+// of list l with below(l, v) true (below is monotone along each list). The lists advance
 // together: every step loads one probe of each list still open before comparing any.
-template <typename F>
+template <int NL, typename F>
 __device__ __forceinline__ void lockstep_search(int32_t* lo, int32_t* hi, const OrdArgs& a, F below) {
   const int32_t* C = a.ws + (int64_t)blockIdx.y * a.Scand;
   for (;;) {
-    int32_t v[kMaxL];
+    int32_t v[NL];
     bool open = false;
 #pragma unroll
-    for (int l = 0; l < kMaxL; ++l) {
+    for (int l = 0; l < NL; ++l) {
       v[l] = 0;
       if (lo[l] < hi[l]) {
         v[l] = C[a.coff[l] + ((lo[l] + hi[l]) >> 1)];
@@ -307,7 +306,7 @@ __device__ __forceinline__ void lockstep_search(int32_t* lo, int32_t* hi, const 
     }
     if (!__builtin_amdgcn_ballot_w64(open)) break;
 #pragma unroll
-    for (int l = 0; l < kMaxL; ++l) {
+    for (int l = 0; l < NL; ++l) {
       if (lo[l] < hi[l]) {
         const int32_t mid = (lo[l] + hi[l]) >> 1;
         if (below(l, v[l])) lo[l] = mid + 1;
@@ -317,6 +316,7 @@ __device__ __forceinline__ void lockstep_search(int32_t* lo, int32_t* hi, const 
   }
 }
 
+template <int NL>  // NL = L
 __global__ void __launch_bounds__(256) order_kernel(OrdArgs a) {
   const int64_t gpos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (gpos >= a.Scand) return;
@@ -333,37 +333,37 @@ __global__ void __launch_bounds__(256) order_kernel(OrdArgs a) {
   const int64_t K = order_key(i, l, a);
   // The binary searches of the L lists run in lockstep: each step issues one independent probe
   // per list, so a thread waits for about log2(max list) loads instead of L times as many.
-  int32_t lo[kMaxL], hi[kMaxL];
+  // In its own list the entry's lower bound is its position (keys of a level increase with i).
+  int32_t lo[NL], hi[NL];
 #pragma unroll
-  for (int l2 = 0; l2 < kMaxL; ++l2) {
-    lo[l2] = 0;
-    hi[l2] = l2 < a.L ? (int32_t)a.cand[l2] : 0;
+  for (int l2 = 0; l2 < NL; ++l2) {
+    lo[l2] = l2 == l ? (int32_t)(gpos - a.coff[l]) : 0;
+    hi[l2] = l2 == l ? lo[l2] : (int32_t)a.cand[l2];
   }
-  lockstep_search(lo, hi, a, [&](int l2, int32_t v) { return order_key(v, l2, a) < K; });
+  lockstep_search<NL>(lo, hi, a, [&](int l2, int32_t v) { return order_key(v, l2, a) < K; });
   int64_t rank = 0;
 #pragma unroll
-  for (int l2 = 0; l2 < kMaxL; ++l2) rank += lo[l2];
+  for (int l2 = 0; l2 < NL; ++l2) rank += lo[l2];
   if (a.replace) {
     // a selected parent is replaced by its children: the children below K are counted at the
     // finer level, so the parents below K (those whose first child is below K) are taken off
-    int32_t lo2[kMaxL], hi2[kMaxL];
-    int32_t bound[kMaxL + 1];  // first entry of list l2 at or after K (or the row count past the end)
+    int32_t lo2[NL], hi2[NL];
+    int32_t bound[NL + 1];  // first entry of list l2 at or after K (or the row count past the end)
 #pragma unroll
-    for (int l2 = 0; l2 <= kMaxL; ++l2) bound[l2] = 0;
+    for (int l2 = 0; l2 <= NL; ++l2) bound[l2] = 0;
 #pragma unroll
-    for (int l2 = 0; l2 < kMaxL; ++l2) {
+    for (int l2 = 0; l2 < NL; ++l2) {
       lo2[l2] = hi2[l2] = 0;
-      if (l2 >= 1 && l2 < a.L) {
+      if (l2 >= 1) {
         const int32_t* c2 = C + a.coff[l2];
         bound[l2] = lo[l2] < a.cand[l2] ? c2[lo[l2]] : (int32_t)a.nrows[l2];
         hi2[l2 - 1] = (int32_t)a.cand[l2 - 1];
       }
     }
     // lists l2 - 1 are searched for bound[l2] * p (slot l2 - 1 of lo2 / hi2)
-    lockstep_search(lo2, hi2, a, [&](int l2, int32_t v) { return (int64_t)v < (int64_t)bound[l2 + 1] * a.p; });
+    lockstep_search<NL>(lo2, hi2, a, [&](int l2, int32_t v) { return (int64_t)v < (int64_t)bound[l2 + 1] * a.p; });
 #pragma unroll
-    for (int l2 = 0; l2 + 1 < kMaxL; ++l2)
-      if (l2 + 1 < a.L) rank -= lo2[l2] / a.p;
+    for (int l2 = 0; l2 + 1 < NL; ++l2) rank -= lo2[l2] / a.p;
   }
   if (rank < 0 || rank >= a.S) return;  // cannot happen for lists written by select_kernel
   a.idx[bh * a.S + rank] = (int32_t)(a.off[l] + i);
@@ -424,6 +424,16 @@ hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_
   for (int l = 0; l < 17; ++l) o.off[l] = s.off[l], o.coff[l] = s.coff[l];
   for (int l = 0; l < 16; ++l) o.pw[l] = s.pw[l], o.cand[l] = s.cand[l], o.nrows[l] = l < s.L ? s.N / s.pw[l] : 0;
   dim3 grid((unsigned)((s.Scand + 255) / 256), (unsigned)BH);
-  hipLaunchKernelGGL(order_kernel, grid, dim3(256), 0, st, o);
+  switch (s.L) {
+    case 1: hipLaunchKernelGGL(order_kernel<1>, grid, dim3(256), 0, st, o); break;
+    case 2: hipLaunchKernelGGL(order_kernel<2>, grid, dim3(256), 0, st, o); break;
+    case 3: hipLaunchKernelGGL(order_kernel<3>, grid, dim3(256), 0, st, o); break;
+    case 4: hipLaunchKernelGGL(order_kernel<4>, grid, dim3(256), 0, st, o); break;
+    case 5: hipLaunchKernelGGL(order_kernel<5>, grid, dim3(256), 0, st, o); break;
+    case 6: hipLaunchKernelGGL(order_kernel<6>, grid, dim3(256), 0, st, o); break;
+    case 7: hipLaunchKernelGGL(order_kernel<7>, grid, dim3(256), 0, st, o); break;
+    case 8: hipLaunchKernelGGL(order_kernel<8>, grid, dim3(256), 0, st, o); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
