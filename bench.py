@@ -317,7 +317,7 @@ def main():
               "over several GPUs (by KV-head group) is not built, so --gpus must be 1.",
               file=sys.stderr)
         raise SystemExit(2)
-    cfg = workloads.CONFIGS[args.config]
+    cfg = {**workloads.CONFIGS, **workloads.SHARD_CONFIGS}[args.config]
     if args.gqa_shared:
         cfg = workloads.scaled(cfg, name=cfg.name + "-gqa-shared", flags=cfg.flags | 4)
     if args.traffic_probe:

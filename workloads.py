@@ -59,6 +59,13 @@ CONFIGS = {
                  notes="iid N(0,1); ~4 GB per tensor"),
 }
 
+# One GPU's share of a configuration sharded by KV group (G query heads and their KV head per
+# GPU, no communication inside the layer): c4 over 8 GPUs.
+SHARD_CONFIGS = {
+    "c4-kv1": Config("c4-kv1", 1, 262144, 4, 1, 128, 4, 5, 4096, "bf16", 1004, "spikes", 0.005,
+                     notes="one GPU's share of c4 over 8 GPUs: one KV head and its 4 query heads"),
+}
+
 # Small shapes for parity tests: several tiles and a ragged tail, oracle in seconds.
 TEST_CONFIGS = {
     # S = 64 + 256 + 1024 + 1024 = 2368 (ragged against 64/128/256-row tiles)
