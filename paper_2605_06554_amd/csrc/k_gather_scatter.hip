@@ -142,6 +142,7 @@ struct RunArgs {
   int32_t nrow[16];                   // N / p^l
   int32_t vec_slots;                  // Ptot % 4 == 0: a head's slot row is 16-byte aligned
   float inv[16];                      // 1 / p^l
+  int32_t rpb;                        // runs per workgroup of a packed launch (else 1)
 };
 
 // Row 0 of source head x of batch b in src, and its slot row.
@@ -562,13 +563,21 @@ struct GroupRun {
   static constexpr int NE = base(L) + RH;  // coarse entries, then RH level-0 entries
 };
 
-template <typename T, int L, int PL, int RHL>
+// PACK: one run has fewer threads of work than a wave (few KV heads), so a workgroup covers
+// a.rpb consecutive runs; the run index then differs between lanes (a separate instantiation,
+// so that the common case keeps a workgroup-uniform run index).
+template <typename T, int L, int PL, int RHL, bool PACK>
 __global__ void __launch_bounds__(256) gather_bwd_group_long_kernel(RunArgs a) {
   using G = GroupRun<PL, RHL, L>;
   constexpr int CH = 16 / sizeof(T);
   constexpr int RH = G::RH, NW = G::NW, NE = G::NE, NC = G::base(L);
-  const uint32_t c = xcd_contiguous(blockIdx.x, gridDim.x);
-  const int hc = blockIdx.y * blockDim.x + threadIdx.x;
+  uint32_t c = xcd_contiguous(blockIdx.x, gridDim.x);
+  int hc = blockIdx.y * blockDim.x + threadIdx.x;
+  if constexpr (PACK) {
+    const int sub = (int)threadIdx.x / a.HC;
+    c = c * (uint32_t)a.rpb + (uint32_t)sub;
+    hc = (int)threadIdx.x - sub * a.HC;
+  }
   if (c >= (uint32_t)a.nruns || hc >= a.HC) return;
   const int h = hc >> a.cpr_shift, cc = hc & ((1 << a.cpr_shift) - 1);
   const int64_t b = blockIdx.z;
@@ -776,9 +785,17 @@ static void launch_gather_bwd_P(const LhShape& s, RunArgs a, dim3 grid, dim3 blo
   } else if (a.Gs > 1 && L > 1 && (s.p == 2 || s.p == 4)) {
     constexpr int RHL = 3;  // runs of 8 positions
     a.nruns = (int32_t)((s.N + 7) / 8);
-    grid.x = (unsigned)((a.nruns + 7) / 8 * 8);
-    if (s.p == 4) hipLaunchKernelGGL((gather_bwd_group_long_kernel<T, L, 2, RHL>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((gather_bwd_group_long_kernel<T, L, 1, RHL>), grid, block, 0, st, a);
+    // under a wave of threads per run: pack runs into one 64-thread workgroup
+    a.rpb = a.HC < 64 ? 64 / a.HC : 1;
+    grid.x = (unsigned)(((a.nruns + a.rpb - 1) / a.rpb + 7) / 8 * 8);
+    if (a.rpb > 1) {
+      block.x = (unsigned)(a.rpb * a.HC);
+      if (s.p == 4) hipLaunchKernelGGL((gather_bwd_group_long_kernel<T, L, 2, RHL, true>), grid, block, 0, st, a);
+      else hipLaunchKernelGGL((gather_bwd_group_long_kernel<T, L, 1, RHL, true>), grid, block, 0, st, a);
+    } else {
+      if (s.p == 4) hipLaunchKernelGGL((gather_bwd_group_long_kernel<T, L, 2, RHL, false>), grid, block, 0, st, a);
+      else hipLaunchKernelGGL((gather_bwd_group_long_kernel<T, L, 1, RHL, false>), grid, block, 0, st, a);
+    }
   } else if (a.Gs > 1 && a.run <= 4) {
     hipLaunchKernelGGL((gather_bwd_group_kernel<T, L, LH_GBWD_GB>), grid, block, 0, st, a);
   } else if (a.run <= 4) {
@@ -844,6 +861,7 @@ static RunArgs run_args(const LhShape& s, const void* src, const int32_t* slot, 
   for (int l = 0; l < 17; ++l) a.off[l] = (int32_t)s.off[l];
   for (int l = 0; l < 16; ++l) a.nrow[l] = l < s.L ? (int32_t)(s.N / s.pw[l]) : 0;
   a.vec_slots = (s.Ptot % 4) == 0;
+  a.rpb = 1;
   return a;
 }
 
