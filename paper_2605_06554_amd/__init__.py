@@ -176,71 +176,153 @@ def lh_last_error() -> str:
     return _load().lh_last_error().decode()
 
 
+# ---------------------------------------------------------------- tensor checks
+# A kernel trusts the sizes the problem implies, so a torch tensor that is too small, strided,
+# on the host or of another dtype is refused here, before its address reaches the library.
+# Raw integer addresses and None are passed through unchecked (the library rejects NULL).
+
+class _Sizes:
+    def __init__(self, pr, S, Ptot):
+        self.B, self.N, self.Hq, self.Hkv, self.D = pr.B, pr.N, pr.Hq, pr.Hkv, pr.D
+        self.S, self.Ptot, self.R, self.Hs = S, Ptot, Ptot - pr.N, selection_heads(pr)
+
+
+_KINDS = {  # element count from the problem's sizes, dtype (None: the problem's)
+    "q": (lambda z: z.B * z.N * z.Hq * z.D, None),
+    "kv": (lambda z: z.B * z.N * z.Hkv * z.D, None),
+    "qpyr": (lambda z: z.B * z.R * z.Hq * z.D, None),
+    "kvpyr": (lambda z: z.B * z.R * z.Hkv * z.D, None),
+    "s_qk": (lambda z: z.B * z.Hq * z.Ptot, torch.float32),
+    "s_kq": (lambda z: z.B * z.Hkv * z.Ptot, torch.float32),
+    "idx": (lambda z: z.B * z.Hs * z.S, torch.int32),
+    "slot": (lambda z: z.B * z.Hs * z.Ptot, torch.int32),
+    "qs": (lambda z: z.B * z.Hq * z.S * z.D, None),
+    "kvs": (lambda z: z.B * z.Hs * z.S * z.D, None),
+    "lse": (lambda z: z.B * z.Hq * z.S, torch.float32),
+    "ws": (lambda z: 0, torch.uint8),
+}
+
+
+def _need(fn, pr, *args):
+    """args: (tensor, argument name, kind) triples for the buffers of entry point fn."""
+    S, Ptot = lh_subseq_len(pr), lh_pyramid_rows(pr)
+    if S < 0 or Ptot < 0:
+        return  # an invalid problem: the library's own check reports it
+    z = _Sizes(pr, S, Ptot)
+    xdt = torch.bfloat16 if pr.dtype == LH_BF16 else torch.float32
+    for t, name, kind in args:
+        if t is None or isinstance(t, int):
+            continue
+        count, dt = _KINDS[kind]
+        dt = xdt if dt is None else dt
+        n = count(z)
+        if not t.is_cuda:
+            raise LighthouseError(f"{fn}: {name} is not a device tensor")
+        if not t.is_contiguous():
+            raise LighthouseError(f"{fn}: {name} is not contiguous")
+        if t.dtype != dt:
+            raise LighthouseError(f"{fn}: {name} has dtype {t.dtype}, {dt} expected")
+        if t.numel() < n:
+            raise LighthouseError(f"{fn}: {name} has {t.numel()} elements, {n} needed")
+
+
 # ---------------------------------------------------------------- stage entry points
 
 def lh_pyramid_pool(pr, q, k, v, qpyr, kpyr, vpyr, stream=None):
+    _need("lh_pyramid_pool", pr, (q, "q", "q"), (k, "k", "kv"), (v, "v", "kv"), (qpyr, "qpyr", "qpyr"),
+          (kpyr, "kpyr", "kvpyr"), (vpyr, "vpyr", "kvpyr"))
     _call("lh_pyramid_pool", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(qpyr), _p(kpyr), _p(vpyr), _stream(stream))
 
 
 def lh_score(pr, q, k, s_qk, s_kq, stream=None):
+    _need("lh_score", pr, (q, "q", "q"), (k, "k", "kv"), (s_qk, "s_qk", "s_qk"), (s_kq, "s_kq", "s_kq"))
     _call("lh_score", ctypes.byref(pr), _p(q), _p(k), _p(s_qk), _p(s_kq), _stream(stream))
 
 
 def lh_pool_score(pr, q, k, v, qpyr, kpyr, vpyr, s_qk, s_kq, stream=None):
+    _need("lh_pool_score", pr, (q, "q", "q"), (k, "k", "kv"), (v, "v", "kv"), (qpyr, "qpyr", "qpyr"),
+          (kpyr, "kpyr", "kvpyr"), (vpyr, "vpyr", "kvpyr"), (s_qk, "s_qk", "s_qk"), (s_kq, "s_kq", "s_kq"))
     _call("lh_pool_score", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(qpyr), _p(kpyr), _p(vpyr), _p(s_qk),
           _p(s_kq), _stream(stream))
 
 
 def lh_select_topk(pr, s_qk, s_kq, idx, slot, ws, ws_bytes=None, stream=None):
+    _need("lh_select_topk", pr, (s_qk, "s_qk", "s_qk"), (s_kq, "s_kq", "s_kq"), (idx, "idx", "idx"),
+          (slot, "slot", "slot"), (ws, "ws", "ws"))
     _call("lh_select_topk", ctypes.byref(pr), _p(s_qk), _p(s_kq), _p(idx), _p(slot), _p(ws),
           _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream))
 
 
 def lh_gather(pr, q, k, v, qpyr, kpyr, vpyr, idx, qs, ks, vs, stream=None):
+    _need("lh_gather", pr, (q, "q", "q"), (k, "k", "kv"), (v, "v", "kv"), (qpyr, "qpyr", "qpyr"),
+          (kpyr, "kpyr", "kvpyr"), (vpyr, "vpyr", "kvpyr"), (idx, "idx", "idx"), (qs, "qs", "qs"),
+          (ks, "ks", "kvs"), (vs, "vs", "kvs"))
     _call("lh_gather", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(qpyr), _p(kpyr), _p(vpyr), _p(idx),
           _p(qs), _p(ks), _p(vs), _stream(stream))
 
 
 def lh_sdpa_fwd(pr, qs, ks, vs, os_, lse, stream=None):
+    _need("lh_sdpa_fwd", pr, (qs, "qs", "qs"), (ks, "ks", "kvs"), (vs, "vs", "kvs"), (os_, "os", "qs"),
+          (lse, "lse", "lse"))
     _call("lh_sdpa_fwd", ctypes.byref(pr), _p(qs), _p(ks), _p(vs), _p(os_), _p(lse), _stream(stream))
 
 
 def lh_sdpa_bwd(pr, qs, ks, vs, os_, lse, dos, dqs, dks, dvs, ws, ws_bytes=None, stream=None):
+    _need("lh_sdpa_bwd", pr, (qs, "qs", "qs"), (ks, "ks", "kvs"), (vs, "vs", "kvs"), (os_, "os", "qs"),
+          (lse, "lse", "lse"), (dos, "dos", "qs"), (dqs, "dqs", "qs"), (dks, "dks", "kvs"), (dvs, "dvs", "kvs"),
+          (ws, "ws", "ws"))
     _call("lh_sdpa_bwd", ctypes.byref(pr), _p(qs), _p(ks), _p(vs), _p(os_), _p(lse), _p(dos), _p(dqs),
           _p(dks), _p(dvs), _p(ws), _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream))
 
 
 def lh_scatter(pr, os_, slot, o, stream=None):
+    _need("lh_scatter", pr, (os_, "os", "qs"), (slot, "slot", "slot"), (o, "o", "q"))
     _call("lh_scatter", ctypes.byref(pr), _p(os_), _p(slot), _p(o), _stream(stream))
 
 
 def lh_scatter_bwd(pr, dout, slot, dos, stream=None):
+    _need("lh_scatter_bwd", pr, (dout, "dout", "q"), (slot, "slot", "slot"), (dos, "dos", "qs"))
     _call("lh_scatter_bwd", ctypes.byref(pr), _p(dout), _p(slot), _p(dos), _stream(stream))
 
 
 def lh_gather_bwd(pr, dqs, dks, dvs, slot, dq, dk, dv, stream=None):
+    _need("lh_gather_bwd", pr, (dqs, "dqs", "qs"), (dks, "dks", "kvs"), (dvs, "dvs", "kvs"),
+          (slot, "slot", "slot"), (dq, "dq", "q"), (dk, "dk", "kv"), (dv, "dv", "kv"))
     _call("lh_gather_bwd", ctypes.byref(pr), _p(dqs), _p(dks), _p(dvs), _p(slot), _p(dq), _p(dk), _p(dv),
           _stream(stream))
 
 
 def lh_attention_fwd(pr, q, k, v, o, idx, slot, qs, ks, vs, os_, lse, ws, ws_bytes=None, stream=None):
+    _need("lh_attention_fwd", pr, (q, "q", "q"), (k, "k", "kv"), (v, "v", "kv"), (o, "o", "q"),
+          (idx, "idx", "idx"), (slot, "slot", "slot"), (qs, "qs", "qs"), (ks, "ks", "kvs"), (vs, "vs", "kvs"),
+          (os_, "os", "qs"), (lse, "lse", "lse"), (ws, "ws", "ws"))
     _call("lh_attention_fwd", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(o), _p(idx), _p(slot), _p(qs), _p(ks),
           _p(vs), _p(os_), _p(lse), _p(ws), _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream))
 
 
 def lh_attention_bwd(pr, idx, slot, qs, ks, vs, os_, lse, dout, dq, dk, dv, ws, ws_bytes=None, stream=None):
+    _need("lh_attention_bwd", pr, (idx, "idx", "idx"), (slot, "slot", "slot"), (qs, "qs", "qs"),
+          (ks, "ks", "kvs"), (vs, "vs", "kvs"), (os_, "os", "qs"), (lse, "lse", "lse"), (dout, "dout", "q"),
+          (dq, "dq", "q"), (dk, "dk", "kv"), (dv, "dv", "kv"), (ws, "ws", "ws"))
     _call("lh_attention_bwd", ctypes.byref(pr), _p(idx), _p(slot), _p(qs), _p(ks), _p(vs), _p(os_), _p(lse),
           _p(dout), _p(dq), _p(dk), _p(dv), _p(ws), _nbytes(ws) if ws_bytes is None else ws_bytes,
           _stream(stream))
 
 
 def lh_sdpa_fwd_indexed(pr, q, k, v, qpyr, kpyr, vpyr, idx, os_, lse, stream=None):
+    _need("lh_sdpa_fwd_indexed", pr, (q, "q", "q"), (k, "k", "kv"), (v, "v", "kv"), (qpyr, "qpyr", "qpyr"),
+          (kpyr, "kpyr", "kvpyr"), (vpyr, "vpyr", "kvpyr"), (idx, "idx", "idx"), (os_, "os", "qs"),
+          (lse, "lse", "lse"))
     _call("lh_sdpa_fwd_indexed", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(qpyr), _p(kpyr), _p(vpyr), _p(idx),
           _p(os_), _p(lse), _stream(stream))
 
 
 def lh_sdpa_bwd_indexed(pr, q, k, v, qpyr, kpyr, vpyr, idx, os_, lse, dos, dqs, dks, dvs, ws, ws_bytes=None,
                         stream=None):
+    _need("lh_sdpa_bwd_indexed", pr, (q, "q", "q"), (k, "k", "kv"), (v, "v", "kv"), (qpyr, "qpyr", "qpyr"),
+          (kpyr, "kpyr", "kvpyr"), (vpyr, "vpyr", "kvpyr"), (idx, "idx", "idx"), (os_, "os", "qs"),
+          (lse, "lse", "lse"), (dos, "dos", "qs"), (dqs, "dqs", "qs"), (dks, "dks", "kvs"), (dvs, "dvs", "kvs"),
+          (ws, "ws", "ws"))
     _call("lh_sdpa_bwd_indexed", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(qpyr), _p(kpyr), _p(vpyr), _p(idx),
           _p(os_), _p(lse), _p(dos), _p(dqs), _p(dks), _p(dvs), _p(ws),
           _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream))
@@ -248,6 +330,9 @@ def lh_sdpa_bwd_indexed(pr, q, k, v, qpyr, kpyr, vpyr, idx, os_, lse, dos, dqs, 
 
 def lh_attention_fwd_indexed(pr, q, k, v, o, idx, slot, qpyr, kpyr, vpyr, os_, lse, ws, ws_bytes=None,
                              stream=None):
+    _need("lh_attention_fwd_indexed", pr, (q, "q", "q"), (k, "k", "kv"), (v, "v", "kv"), (o, "o", "q"),
+          (idx, "idx", "idx"), (slot, "slot", "slot"), (qpyr, "qpyr", "qpyr"), (kpyr, "kpyr", "kvpyr"),
+          (vpyr, "vpyr", "kvpyr"), (os_, "os", "qs"), (lse, "lse", "lse"), (ws, "ws", "ws"))
     _call("lh_attention_fwd_indexed", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(o), _p(idx), _p(slot),
           _p(qpyr), _p(kpyr), _p(vpyr), _p(os_), _p(lse), _p(ws), _nbytes(ws) if ws_bytes is None else ws_bytes,
           _stream(stream))
@@ -255,6 +340,10 @@ def lh_attention_fwd_indexed(pr, q, k, v, o, idx, slot, qpyr, kpyr, vpyr, os_, l
 
 def lh_attention_bwd_indexed(pr, q, k, v, qpyr, kpyr, vpyr, idx, slot, os_, lse, dout, dq, dk, dv, ws,
                              ws_bytes=None, stream=None):
+    _need("lh_attention_bwd_indexed", pr, (q, "q", "q"), (k, "k", "kv"), (v, "v", "kv"),
+          (qpyr, "qpyr", "qpyr"), (kpyr, "kpyr", "kvpyr"), (vpyr, "vpyr", "kvpyr"), (idx, "idx", "idx"),
+          (slot, "slot", "slot"), (os_, "os", "qs"), (lse, "lse", "lse"), (dout, "dout", "q"), (dq, "dq", "q"),
+          (dk, "dk", "kv"), (dv, "dv", "kv"), (ws, "ws", "ws"))
     _call("lh_attention_bwd_indexed", ctypes.byref(pr), _p(q), _p(k), _p(v), _p(qpyr), _p(kpyr), _p(vpyr),
           _p(idx), _p(slot), _p(os_), _p(lse), _p(dout), _p(dq), _p(dk), _p(dv), _p(ws),
           _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream))

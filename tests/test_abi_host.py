@@ -144,3 +144,44 @@ def test_indexed_forward_workspace_is_the_scores_and_lists():
     R = lh.lh_pyramid_rows(pr) - 4096
     al = lambda n: (n + 255) // 256 * 256
     assert full - idx == al(2 * R * 4 * 128 * 2) + 2 * al(2 * R * 2 * 128 * 2)
+
+
+class _FakeDeviceTensor:
+    """Stands in for a device tensor on a host without a GPU (only what the binding reads)."""
+
+    def __init__(self, n, dtype, contiguous=True):
+        self.n, self.dtype, self.contiguous, self.is_cuda = n, dtype, contiguous, True
+
+    def numel(self):
+        return self.n
+
+    def is_contiguous(self):
+        return self.contiguous
+
+
+def test_binding_refuses_bad_tensors_before_the_library():
+    """The Python binding checks device, layout, dtype and size of every tensor against the
+    problem before passing its address on: a short buffer would otherwise be read or written
+    past its end by a kernel."""
+    import torch
+    pr = _pr(dtype=lh.LH_BF16, B=1, N=1024, Hq=2, Hkv=1, D=64, p=4, L=3, k=16)
+    S = lh.lh_subseq_len(pr)
+    n_qs, n_kvs, n_lse = 2 * S * 64, 2 * S * 64, 2 * S  # selection heads = Hq = 2
+    good = lambda n, dt=torch.bfloat16: _FakeDeviceTensor(n, dt)
+    ok = (good(n_qs), good(n_kvs), good(n_kvs), good(n_qs), good(n_lse, torch.float32))
+    cases = [
+        ((torch.zeros(4),) + ok[1:], "not a device tensor"),
+        ((_FakeDeviceTensor(n_qs, torch.bfloat16, False),) + ok[1:], "not contiguous"),
+        ((good(n_qs, torch.float32),) + ok[1:], "dtype"),
+        (ok[:1] + (good(n_kvs - 1),) + ok[2:], "elements"),
+        (ok[:4] + (good(n_lse - 1, torch.float32),), "elements"),
+    ]
+    for args, msg in cases:
+        with pytest.raises(lh.LighthouseError, match=msg):
+            lh.lh_sdpa_fwd(pr, *args)
+    # with GQA-shared selection, ks and vs hold one row block per KV head
+    prs = _pr(dtype=lh.LH_BF16, B=1, N=1024, Hq=2, Hkv=1, D=64, p=4, L=3, k=16, flags=lh.LH_FLAG_GQA_SHARED)
+    Ss = lh.lh_subseq_len(prs)
+    with pytest.raises(lh.LighthouseError, match="ks has"):
+        lh.lh_sdpa_fwd(prs, good(2 * Ss * 64), good(Ss * 64 - 1), good(Ss * 64), good(2 * Ss * 64),
+                       good(2 * Ss, torch.float32))
