@@ -305,7 +305,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=512)
+    ap.add_argument("--cpu-rows", type=int, default=16384,
+                    help="gathered rows of the oracle's SDPA sample (the cpu_baseline leg)")
     ap.add_argument("--gqa-shared", action="store_true",
                     help="one selection per KV group (LH_FLAG_GQA_SHARED) instead of one per query head")
     ap.add_argument("--traffic-probe", action="store_true",
