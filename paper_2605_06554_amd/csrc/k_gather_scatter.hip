@@ -116,7 +116,7 @@ __global__ void __launch_bounds__(256) gather_kernel(GatherArgs a) {
     sk = reinterpret_cast<const T*>(a.kp) + ((b * a.R + r) * a.Hkv + g) * a.D;
     sv = reinterpret_cast<const T*>(a.vp) + ((b * a.R + r) * a.Hkv + g) * a.D;
   }
-  const u32x4 xq = load_raw(sq + cc * CH);
+  const u32x4 xq = load16_nt(sq + cc * CH);  // a query row is gathered once; K, V rows by every head of the group
   store16_nt(reinterpret_cast<T*>(a.qs) + o, xq);
   if (kv_out) {
     const u32x4 xk = load_raw(sk + cc * CH);
@@ -707,7 +707,7 @@ __global__ void __launch_bounds__(256) scatter_bwd_kernel(ScatterBwdArgs a) {
     for (int r = 0; r < RB; ++r) {
       const int32_t u = u0 + ub + r;
       const bool valid = ub + r < nu && u >= 1 && u <= a.N;
-      v[r] = valid ? load_raw(src + (int64_t)(u - 1) * sstride) : u32x4{0, 0, 0, 0};
+      v[r] = valid ? load16_nt(src + (int64_t)(u - 1) * sstride) : u32x4{0, 0, 0, 0};  // dout: read once
       m0[r] = valid ? sl[u - 1] : -1;
     }
 #pragma unroll

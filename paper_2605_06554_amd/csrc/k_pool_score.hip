@@ -188,7 +188,7 @@ __global__ void __launch_bounds__(256) pool_score_kernel(PoolArgs a) {
     u32x4 v[kPoolRB];
 #pragma unroll
     for (int r = 0; r < kPoolRB; ++r) {
-      if (r < nr && active) v[r] = *reinterpret_cast<const u32x4*>(xrow + (int64_t)(rb + r) * xstride);
+      if (r < nr && active) v[r] = load16_nt(xrow + (int64_t)(rb + r) * xstride);
       else v[r] = u32x4{0, 0, 0, 0};
     }
     if (any_score && active && srow_base) {

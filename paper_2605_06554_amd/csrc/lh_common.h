@@ -90,6 +90,13 @@ __device__ __forceinline__ void store16_nt(void* p, const u32x4& o) {
   const u32x4v x = {o.x, o.y, o.z, o.w};
   __builtin_nontemporal_store(x, reinterpret_cast<u32x4v*>(p));
 }
+// 16-byte load with the non-temporal hint, for input chunks a kernel reads exactly once.
+__device__ __forceinline__ u32x4 load16_nt(const void* p) {
+  const u32x4v x = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p));
+  u32x4 o;
+  o.x = x.x, o.y = x.y, o.z = x.z, o.w = x.w;
+  return o;
+}
 __device__ __forceinline__ void store_chunk_f32(float* p, const float* v) {
   u32x4 o;
   o.x = __float_as_uint(v[0]), o.y = __float_as_uint(v[1]), o.z = __float_as_uint(v[2]), o.w = __float_as_uint(v[3]);
