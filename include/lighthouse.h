@@ -121,7 +121,7 @@ typedef struct {
   int32_t L;        /* pyramid levels, >= 1 (L = 1 is plain causal SDPA)                 */
   int32_t k;        /* parents per level per (batch, query head), >= 0                   */
   int32_t dtype;    /* lh_dtype of every Q/K/V/O-like tensor and gradient                */
-  float scale;      /* softmax scale; 0 selects 1/sqrt(D)                                */
+  float scale;      /* softmax scale, finite and >= 0; 0 selects 1/sqrt(D)               */
   uint32_t flags;   /* LH_FLAG_* bits                                                    */
 } lh_problem;
 

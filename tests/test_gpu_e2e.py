@@ -6,7 +6,7 @@ import torch
 
 import oracle
 import workloads
-from parity import check_close, check_close_heads, check_equal
+from parity import check_close, check_equal, check_layer
 
 lh = pytest.importorskip("paper_2605_06554_amd")
 
@@ -31,22 +31,20 @@ def test_layer_matches_oracle(name):
     c = _cfg(name)
     print(f"[e2e] {name}", flush=True)
     inp = workloads.make_inputs(c)
-    pr, st, (dq, dk, dv) = _run(c, inp)
-    q, k, v = (inp[x].double().numpy() for x in ("q", "k", "v"))
-    odt = oracle.BF16 if c.dtype == "bf16" else oracle.F32
-    f = oracle.layer_forward(q, k, v, c.p, c.L, c.k, dtype=odt, flags=c.flags)
-    g = oracle.layer_backward(f, inp["dout"].double().numpy())
-    check_equal("idx", st["idx"], f["idx"])
-    check_equal("slot", st["slot"], f["slot"])
-    check_equal("qs", st["qs"].double(), f["qs"])
-    check_equal("ks", st["ks"].double(), f["ks"])
-    check_equal("vs", st["vs"].double(), f["vs"])
-    check_close_heads("os", st["os"], f["os"], c.dtype, 1)
-    check_close("lse", st["lse"], f["lse"], "fp32")
-    check_close_heads("o", st["o"], f["o"], c.dtype, 2)
-    check_close_heads("dq", dq, g["dq"], c.dtype, 2)
-    check_close_heads("dk", dk, g["dk"], c.dtype, 2)
-    check_close_heads("dv", dv, g["dv"], c.dtype, 2)
+    pr, st, grads = _run(c, inp)
+    check_layer(c, inp, st, grads)
+
+
+@pytest.mark.timeout(600)
+def test_c2_layer_matches_oracle():
+    """Config c2 (16 heads, N = 16,384, planted key spikes, S = 13,568) in full: every head and
+    every row of every output against the oracle."""
+    c = workloads.CONFIGS["c2"]
+    print("[e2e] c2", flush=True)
+    inp = workloads.make_inputs(c)
+    pr, st, grads = _run(c, inp)
+    assert lh.lh_subseq_len(pr) == 13568
+    check_layer(c, inp, st, grads)
 
 
 def test_full_budget_replace_mode_is_dense_sdpa():

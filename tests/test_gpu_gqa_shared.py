@@ -6,7 +6,7 @@ import torch
 
 import oracle
 import workloads
-from parity import check_close, check_close_heads, check_equal
+from parity import check_equal, check_layer
 
 lh = pytest.importorskip("paper_2605_06554_amd")
 
@@ -24,21 +24,7 @@ def test_shared_layer_matches_oracle(name):
     dq, dk, dv = lh.attention_backward(pr, st, dout)
     torch.cuda.synchronize()
     assert st["idx"].shape[1] == c.Hkv and st["ks"].shape[1] == c.Hkv
-    odt = oracle.BF16 if c.dtype == "bf16" else oracle.F32
-    f = oracle.layer_forward(*(inp[x].double().numpy() for x in ("q", "k", "v")), c.p, c.L, c.k, dtype=odt,
-                             flags=c.flags)
-    g = oracle.layer_backward(f, inp["dout"].double().numpy())
-    check_equal("idx", st["idx"], f["idx"])
-    check_equal("slot", st["slot"], f["slot"])
-    check_equal("qs", st["qs"].double(), f["qs"])
-    check_equal("ks", st["ks"].double(), f["ks"])
-    check_equal("vs", st["vs"].double(), f["vs"])
-    check_close_heads("os", st["os"], f["os"], c.dtype, 1)
-    check_close("lse", st["lse"], f["lse"], "fp32")
-    check_close_heads("o", st["o"], f["o"], c.dtype, 2)
-    check_close_heads("dq", dq, g["dq"], c.dtype, 2)
-    check_close_heads("dk", dk, g["dk"], c.dtype, 2)
-    check_close_heads("dv", dv, g["dv"], c.dtype, 2)
+    check_layer(c, inp, st, (dq, dk, dv))
 
 
 def test_shared_indexed_layer_is_bitwise_the_materialised_layer():

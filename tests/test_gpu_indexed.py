@@ -7,7 +7,7 @@ import torch
 
 import oracle
 import workloads
-from parity import check_close_heads, check_equal
+from parity import check_close_heads, check_equal, check_layer
 
 lh = pytest.importorskip("paper_2605_06554_amd")
 
@@ -48,6 +48,20 @@ def test_indexed_layer_is_bitwise_the_materialised_layer(name):
     _same("dq", dqi, dq)
     _same("dk", dki, dk)
     _same("dv", dvi, dv)
+
+
+@pytest.mark.parametrize("name", ["t_gqa", "t_p3", "t_strat", "t_g3"])
+def test_indexed_layer_matches_oracle(name):
+    """The indexed layer's own outputs (forward and backward) against the oracle, at the same
+    bar as the materialised layer."""
+    c = _cfg(name)
+    print(f"[indexed vs oracle] {name}", flush=True)
+    inp = workloads.make_inputs(c)
+    q, k, v, dout = (inp[x].to(DEV) for x in ("q", "k", "v", "dout"))
+    pri, sti = lh.attention_forward_indexed(q, k, v, c.p, c.L, c.k, flags=c.flags)
+    grads = lh.attention_backward_indexed(pri, q, k, v, sti, dout)
+    torch.cuda.synchronize()
+    check_layer(c, inp, sti, grads)
 
 
 def test_indexed_stage_calls_match_gathered_rows():

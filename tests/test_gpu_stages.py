@@ -7,9 +7,10 @@ import numpy as np
 import pytest
 import torch
 
+import bf16_floor
 import oracle
 import workloads
-from parity import check_close, check_equal, to64
+from parity import check_close, check_equal, rounding_floor, to64
 
 lh = pytest.importorskip("paper_2605_06554_amd")
 
@@ -194,10 +195,17 @@ def test_gather_sdpa_scatter_stages(name):
     lse = torch.empty(c.B, c.Hq, S, dtype=torch.float32, device=DEV)
     lh.lh_sdpa_fwd(pr, qs, ks, vs, os_, lse)
     torch.cuda.synchronize()
+    sc = f["scale"]
+    bf = c.dtype == "bf16"
+    os_emu = {}
     for b in range(c.B):
         for hq in range(c.Hq):
-            check_close(f"os[{b},{hq}]", os_[b, hq], f["os"][b, hq], c.dtype)
-    check_close("lse", lse, f["lse"], "fp32")
+            fl = None
+            if bf:
+                os_emu[b, hq], _ = bf16_floor.sdpa_fwd(f["qs"][b, hq], f["ks"][b, hq], f["vs"][b, hq], sc)
+                fl = np.abs(os_emu[b, hq] - f["os"][b, hq]).max()
+            check_close(f"os[{b},{hq}]", os_[b, hq], f["os"][b, hq], c.dtype, fl)
+            check_close(f"lse[{b},{hq}]", lse[b, hq], f["lse"][b, hq], "fp32")
     # scatter of the oracle's own sub-sequence output (rounded to the dtype) isolates the scatter
     os_ref = torch.from_numpy(f["os"]).to(dt).to(DEV)
     o = torch.empty_like(q)
@@ -207,27 +215,33 @@ def test_gather_sdpa_scatter_stages(name):
     for b in range(c.B):
         for hq in range(c.Hq):
             ref = oracle.scatter(h, f["idx"][b, hq], to64(os_ref[b, hq]))
-            check_close(f"o[{b},{hq}]", o[b, :, hq], ref, c.dtype)
+            check_close(f"o[{b},{hq}]", o[b, :, hq], ref, c.dtype, rounding_floor(ref) if bf else None)
     dos = torch.empty(c.B, c.Hq, S, c.D, dtype=dt, device=DEV)
     lh.lh_scatter_bwd(pr, dout, slot, dos)
     torch.cuda.synchronize()
     for b in range(c.B):
         for hq in range(c.Hq):
-            check_close(f"dos[{b},{hq}]", dos[b, hq], g["dos"][b, hq], c.dtype)
+            check_close(f"dos[{b},{hq}]", dos[b, hq], g["dos"][b, hq], c.dtype,
+                        rounding_floor(g["dos"][b, hq]) if bf else None)
     # SDPA backward on the oracle's inputs (os/lse from the GPU forward)
     dqs, dks, dvs = (torch.empty(c.B, c.Hq, S, c.D, dtype=dt, device=DEV) for _ in range(3))
     dos_ref = torch.from_numpy(g["dos"]).to(dt).to(DEV)
     ws = lh.workspace(pr, lh.LH_OP_SDPA_BWD)
     lh.lh_sdpa_bwd(pr, qs, ks, vs, os_, lse, dos_ref, dqs, dks, dvs, ws)
     torch.cuda.synchronize()
-    sc = f["scale"]
     for b in range(c.B):
         for hq in range(c.Hq):
-            rq, rk, rv = oracle.sdpa_bwd(f["qs"][b, hq], f["ks"][b, hq], f["vs"][b, hq], f["os"][b, hq],
-                                         f["lse"][b, hq], to64(dos_ref[b, hq]), sc)
-            check_close(f"dqs[{b},{hq}]", dqs[b, hq], rq, c.dtype)
-            check_close(f"dks[{b},{hq}]", dks[b, hq], rk, c.dtype)
-            check_close(f"dvs[{b},{hq}]", dvs[b, hq], rv, c.dtype)
+            args = (f["qs"][b, hq], f["ks"][b, hq], f["vs"][b, hq])
+            rq, rk, rv = oracle.sdpa_bwd(*args, f["os"][b, hq], f["lse"][b, hq], to64(dos_ref[b, hq]), sc)
+            fq = fk = fv = None
+            if bf:
+                eq, ek, ev = bf16_floor.sdpa_bwd(*args, os_emu[b, hq], f["lse"][b, hq], to64(dos_ref[b, hq]), sc)
+                fq = np.abs(eq - rq).max()
+                fk = np.abs(bf16_floor.round_bf16(ek) - rk).max()
+                fv = np.abs(bf16_floor.round_bf16(ev) - rv).max()
+            check_close(f"dqs[{b},{hq}]", dqs[b, hq], rq, c.dtype, fq)
+            check_close(f"dks[{b},{hq}]", dks[b, hq], rk, c.dtype, fk)
+            check_close(f"dvs[{b},{hq}]", dvs[b, hq], rv, c.dtype, fv)
     # gather + pool backward on the oracle's sub-sequence gradients
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     dqs_r, dks_r, dvs_r = (torch.from_numpy(g[x]).to(dt).to(DEV) for x in ("dqs", "dks", "dvs"))
@@ -237,15 +251,15 @@ def test_gather_sdpa_scatter_stages(name):
     for b in range(c.B):
         for hq in range(c.Hq):
             ref = oracle.gather_pool_bwd(h, f["idx"][b, hq], to64(dqs_r[b, hq]))
-            check_close(f"dq[{b},{hq}]", dq[b, :, hq], ref, c.dtype)
+            check_close(f"dq[{b},{hq}]", dq[b, :, hq], ref, c.dtype, rounding_floor(ref) if bf else None)
         for gg in range(c.Hkv):
             rk = np.zeros((c.N, c.D))
             rv = np.zeros((c.N, c.D))
             for hq in range(gg * G, (gg + 1) * G):
                 oracle.gather_pool_bwd(h, f["idx"][b, hq], to64(dks_r[b, hq]), rk)
                 oracle.gather_pool_bwd(h, f["idx"][b, hq], to64(dvs_r[b, hq]), rv)
-            check_close(f"dk[{b},{gg}]", dk[b, :, gg], rk, c.dtype)
-            check_close(f"dv[{b},{gg}]", dv[b, :, gg], rv, c.dtype)
+            check_close(f"dk[{b},{gg}]", dk[b, :, gg], rk, c.dtype, rounding_floor(rk) if bf else None)
+            check_close(f"dv[{b},{gg}]", dv[b, :, gg], rv, c.dtype, rounding_floor(rv) if bf else None)
 
 
 @pytest.mark.parametrize("S,D,dt", [(1, 128, "bf16"), (31, 64, "bf16"), (300, 128, "bf16"), (1000, 64, "bf16"),
@@ -269,9 +283,18 @@ def test_sdpa_standalone(S, D, dt, rng):
     for hh in range(H):
         a = [t[0, hh].double().numpy() for t in x]
         ro, rl = oracle.sdpa_fwd(a[0], a[1], a[2], sc)
-        check_close(f"os[{hh}]", os_[0, hh], ro, dt)
+        fo = fq = fk = fv = None
+        if dt == "bf16":
+            eo, _ = bf16_floor.sdpa_fwd(a[0], a[1], a[2], sc)
+            fo = np.abs(eo - ro).max()
+        check_close(f"os[{hh}]", os_[0, hh], ro, dt, fo)
         check_close(f"lse[{hh}]", lse[0, hh], rl, "fp32")
         rq, rk, rv = oracle.sdpa_bwd(a[0], a[1], a[2], ro, rl, a[3], sc)
-        check_close(f"dqs[{hh}]", dqs[0, hh], rq, dt)
-        check_close(f"dks[{hh}]", dks[0, hh], rk, dt)
-        check_close(f"dvs[{hh}]", dvs[0, hh], rv, dt)
+        if dt == "bf16":
+            eq, ek, ev = bf16_floor.sdpa_bwd(a[0], a[1], a[2], eo, rl, a[3], sc)
+            fq = np.abs(eq - rq).max()
+            fk = np.abs(bf16_floor.round_bf16(ek) - rk).max()
+            fv = np.abs(bf16_floor.round_bf16(ev) - rv).max()
+        check_close(f"dqs[{hh}]", dqs[0, hh], rq, dt, fq)
+        check_close(f"dks[{hh}]", dks[0, hh], rk, dt, fk)
+        check_close(f"dvs[{hh}]", dvs[0, hh], rv, dt, fv)
