@@ -14,7 +14,8 @@ that bf16 rounding alone produces, reported beside the raw error (``bf16_floor.p
     every element must satisfy |gpu - ref| <= 2 * |bf16(ref) - ref| (or the raw bar);
   * the attention and the whole layer have the floor of an emulation that performs exactly the
     design's roundings (stored tensors, and the softmax weights and dS before their products) in
-    otherwise exact arithmetic: per head slice, max |gpu - ref| <= 2 * max |emulated - ref|.
+    otherwise exact arithmetic: per head slice, max |gpu - ref| <= 2 * floor, where floor is
+    the larger of max |emulated - ref| and half a bf16 ulp of the slice's largest |ref|.
 A wrong mask, index, scale or dropped term gives errors the size of the values themselves, tens
 to hundreds of times these floors. No fp32 tensor is given a floor.
 
@@ -47,6 +48,19 @@ def rounding_floor(ref) -> np.ndarray:
     """Element-wise distance of the exact values to their bf16 rounding (nearest even)."""
     r = np.asarray(ref, np.float64)
     return np.abs(torch.from_numpy(r).to(torch.bfloat16).double().numpy() - r)
+
+
+def emulated_floor(emu, ref) -> float:
+    """The bf16 floor of a tensor from its emulation: the emulation's max-abs distance to the
+    oracle, and at least half a bf16 unit in the last place of the tensor's largest value (the
+    worst case of storing that value, which one realisation of the roundings can miss)."""
+    e = np.asarray(emu, np.float64)
+    r = np.asarray(ref, np.float64)
+    if not r.size:
+        return 0.0
+    m = float(np.abs(r).max())
+    half_ulp = 2.0 ** (np.floor(np.log2(m)) - 8) if m > 0 else 0.0
+    return max(float(np.abs(e - r).max()), half_ulp)
 
 
 def check_close(name, gpu, ref, dtype, floor=None):
@@ -99,7 +113,7 @@ def check_close_heads(name, gpu, ref, dtype, head_axis, emu=None, floor=None):
             fl = None
             if emu is not None:
                 es = np.take(np.asarray(emu, np.float64)[b], h, axis=head_axis - 1)
-                fl = float(np.abs(es - rs).max()) if rs.size else 0.0
+                fl = emulated_floor(es, rs)
             elif floor is not None:
                 fl = np.take(np.asarray(floor, np.float64)[b], h, axis=head_axis - 1)
             worst = max(worst, check_close(f"{name}[{b},{h}]", gs, rs, dtype, fl))

@@ -28,7 +28,7 @@ import torch
 import bf16_floor
 import oracle
 import workloads
-from parity import check_close, check_equal
+from parity import check_close, check_equal, emulated_floor
 
 pytestmark = pytest.mark.gpu
 
@@ -152,10 +152,10 @@ def test_c4_group_every_row(t):
     hq = C4_GROUP * (L["cfg"].Hq // L["cfg"].Hkv) + t
     r = _c4_head(hq)
     st = L["st"]
-    check_close(f"c4 os[0,{hq}]", _host(st["os"][0, hq]), r["os"], "bf16", np.abs(r["e_os"] - r["os"]).max())
+    check_close(f"c4 os[0,{hq}]", _host(st["os"][0, hq]), r["os"], "bf16", emulated_floor(r["e_os"], r["os"]))
     check_close(f"c4 lse[0,{hq}]", st["lse"][0, hq].double().cpu().numpy(), r["lse"], "fp32")
-    check_close(f"c4 o[0,{hq}]", _host(st["o"][0, :, hq]), r["o"], "bf16", np.abs(r["e_o"] - r["o"]).max())
-    check_close(f"c4 dq[0,{hq}]", _host(L["dq"][0, :, hq]), r["dq"], "bf16", np.abs(r["e_dq"] - r["dq"]).max())
+    check_close(f"c4 o[0,{hq}]", _host(st["o"][0, :, hq]), r["o"], "bf16", emulated_floor(r["e_o"], r["o"]))
+    check_close(f"c4 dq[0,{hq}]", _host(L["dq"][0, :, hq]), r["dq"], "bf16", emulated_floor(r["e_dq"], r["dq"]))
     print(f"[fullsize] c4 head {hq}: every row checked", flush=True)
 
 
@@ -168,7 +168,7 @@ def test_c4_group_dk_dv_every_row():
     for nm in ("dk", "dv"):
         ref = sum(r[nm] for r in rs)
         emu = bf16_floor.round_bf16(sum(r["e_" + nm] for r in rs))
-        check_close(f"c4 {nm}[0,{C4_GROUP}]", _host(L[nm][0, :, C4_GROUP]), ref, "bf16", np.abs(emu - ref).max())
+        check_close(f"c4 {nm}[0,{C4_GROUP}]", _host(L[nm][0, :, C4_GROUP]), ref, "bf16", emulated_floor(emu, ref))
 
 
 # ------------------------------------------------------------------ c3, c5: sampled positions
@@ -248,14 +248,14 @@ def test_full_size_sampled_parity(name):
         e_dos = bf16_floor.round_bf16(dos)
         e_dqs, _, _ = bf16_floor.sdpa_bwd(qs, ks, vs, e_os, e_lse, e_dos, sc, qrows=rows, krange=(S, S))
         check_close(f"{name} os[{b},{hq}]", _host(st["os"][b, hq])[rows], os_ref[rows], "bf16",
-                    np.abs(e_os[rows] - os_ref[rows]).max())
+                    emulated_floor(e_os[rows], os_ref[rows]))
         check_close(f"{name} lse[{b},{hq}]", st["lse"][b, hq].double().cpu().numpy()[rows], lse_ref[rows], "fp32")
         o_ref = oracle.scatter(h, idx, os_ref)[j_sample]
         e_o = bf16_floor.round_bf16(oracle.scatter(h, idx, e_os)[j_sample])
         dq_ref = oracle.gather_pool_bwd(h, idx, dqs_ref)[j_sample]
         e_dq = bf16_floor.round_bf16(oracle.gather_pool_bwd(h, idx, e_dqs)[j_sample])
-        check_close(f"{name} o[{b},{hq}]", _host(st["o"][b, :, hq][jt_]), o_ref, "bf16", np.abs(e_o - o_ref).max())
-        check_close(f"{name} dq[{b},{hq}]", _host(L["dq"][b, :, hq][jt_]), dq_ref, "bf16", np.abs(e_dq - dq_ref).max())
+        check_close(f"{name} o[{b},{hq}]", _host(st["o"][b, :, hq][jt_]), o_ref, "bf16", emulated_floor(e_o, o_ref))
+        check_close(f"{name} dq[{b},{hq}]", _host(L["dq"][b, :, hq][jt_]), dq_ref, "bf16", emulated_floor(e_dq, dq_ref))
         print(f"[fullsize] {name} head ({b},{hq}): {len(rows)} rows evaluated", flush=True)
     # dK, dV of the checked KV group at the last base positions (G = 1 at c3 and c5)
     assert cfg.Hq == cfg.Hkv
@@ -279,7 +279,7 @@ def _check_dkdv(name, L, b, g, idx, jt, dks, dvs, e_dks, e_dvs):
         ref = oracle.gather_pool_bwd(h, idx, ref_s)[jt]
         emu = bf16_floor.round_bf16(oracle.gather_pool_bwd(h, idx, bf16_floor.round_bf16(emu_s))[jt])
         check_close(f"{name} {nm}[{b},{g}] ({len(jt)} positions)", _host(L[nm][b, :, g][jt_]), ref, "bf16",
-                    np.abs(emu - ref).max())
+                    emulated_floor(emu, ref))
 
 
 @pytest.mark.timeout(900)

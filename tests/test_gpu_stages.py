@@ -10,7 +10,7 @@ import torch
 import bf16_floor
 import oracle
 import workloads
-from parity import check_close, check_equal, rounding_floor, to64
+from parity import check_close, check_equal, emulated_floor, rounding_floor, to64
 
 lh = pytest.importorskip("paper_2605_06554_amd")
 
@@ -203,7 +203,7 @@ def test_gather_sdpa_scatter_stages(name):
             fl = None
             if bf:
                 os_emu[b, hq], _ = bf16_floor.sdpa_fwd(f["qs"][b, hq], f["ks"][b, hq], f["vs"][b, hq], sc)
-                fl = np.abs(os_emu[b, hq] - f["os"][b, hq]).max()
+                fl = emulated_floor(os_emu[b, hq], f["os"][b, hq])
             check_close(f"os[{b},{hq}]", os_[b, hq], f["os"][b, hq], c.dtype, fl)
             check_close(f"lse[{b},{hq}]", lse[b, hq], f["lse"][b, hq], "fp32")
     # scatter of the oracle's own sub-sequence output (rounded to the dtype) isolates the scatter
@@ -236,9 +236,9 @@ def test_gather_sdpa_scatter_stages(name):
             fq = fk = fv = None
             if bf:
                 eq, ek, ev = bf16_floor.sdpa_bwd(*args, os_emu[b, hq], f["lse"][b, hq], to64(dos_ref[b, hq]), sc)
-                fq = np.abs(eq - rq).max()
-                fk = np.abs(bf16_floor.round_bf16(ek) - rk).max()
-                fv = np.abs(bf16_floor.round_bf16(ev) - rv).max()
+                fq = emulated_floor(eq, rq)
+                fk = emulated_floor(bf16_floor.round_bf16(ek), rk)
+                fv = emulated_floor(bf16_floor.round_bf16(ev), rv)
             check_close(f"dqs[{b},{hq}]", dqs[b, hq], rq, c.dtype, fq)
             check_close(f"dks[{b},{hq}]", dks[b, hq], rk, c.dtype, fk)
             check_close(f"dvs[{b},{hq}]", dvs[b, hq], rv, c.dtype, fv)
@@ -286,15 +286,15 @@ def test_sdpa_standalone(S, D, dt, rng):
         fo = fq = fk = fv = None
         if dt == "bf16":
             eo, _ = bf16_floor.sdpa_fwd(a[0], a[1], a[2], sc)
-            fo = np.abs(eo - ro).max()
+            fo = emulated_floor(eo, ro)
         check_close(f"os[{hh}]", os_[0, hh], ro, dt, fo)
         check_close(f"lse[{hh}]", lse[0, hh], rl, "fp32")
         rq, rk, rv = oracle.sdpa_bwd(a[0], a[1], a[2], ro, rl, a[3], sc)
         if dt == "bf16":
             eq, ek, ev = bf16_floor.sdpa_bwd(a[0], a[1], a[2], eo, rl, a[3], sc)
-            fq = np.abs(eq - rq).max()
-            fk = np.abs(bf16_floor.round_bf16(ek) - rk).max()
-            fv = np.abs(bf16_floor.round_bf16(ev) - rv).max()
+            fq = emulated_floor(eq, rq)
+            fk = emulated_floor(bf16_floor.round_bf16(ek), rk)
+            fv = emulated_floor(bf16_floor.round_bf16(ev), rv)
         check_close(f"dqs[{hh}]", dqs[0, hh], rq, dt, fq)
         check_close(f"dks[{hh}]", dks[0, hh], rk, dt, fk)
         check_close(f"dvs[{hh}]", dvs[0, hh], rv, dt, fv)
