@@ -49,6 +49,8 @@ def _pr(**kw):
     (dict(N=0), -2),
     (dict(L=1, p=0), 0),                # p is irrelevant with one level
     (dict(N=2 ** 20, L=2, k=1000), -3),  # one level would rank 262144 candidates
+    (dict(scale=-0.125), -3),           # a negative softmax scale is refused
+    (dict(scale=float("nan")), -3),
 ])
 def test_check_codes(kw, code):
     pr = _pr(**kw)
