@@ -197,6 +197,18 @@ lh_status lh_sdpa_bwd(const lh_problem* pr, const void* qs, const void* ks, cons
                       const void* os, const float* lse, const void* dos,
                       void* dqs, void* dks, void* dvs, void* ws, size_t ws_bytes, void* stream);
 
+/* lh_sdpa_bwd for callers that cannot allocate device memory (code under HIP graph capture,
+   tight serving loops, harnesses that forbid allocation): the same computation and bits, with
+   Delta kept in a static device array of the library instead of a caller workspace. No
+   allocation or free happens in the call. Limit: B * Hq * S <= 4,194,304 (16 MiB of fp32);
+   larger problems get LH_E_WORKSPACE before anything is enqueued. Each GPU the library runs on
+   holds its own 16 MiB copy until the process ends. Every call on a GPU shares that GPU's
+   array, so calls that overlap on one GPU (other streams, other threads) race; serialise them.
+   The array needs no clearing: each call overwrites what it reads. */
+lh_status lh_sdpa_bwd_noalloc(const lh_problem* pr, const void* qs, const void* ks, const void* vs,
+                              const void* os, const float* lse, const void* dos,
+                              void* dqs, void* dks, void* dvs, void* stream);
+
 /* Sec. 3.6, Eqs. fanout and scatter: entry (l, i) at position m writes os[m] to base
    positions R(l,i) = [(i+1) p^l - 1, (i+2) p^l - 2] (clipped at N-1); contributions of
    different levels are summed in fp32 (level L-1 first) and rounded once. Base positions

@@ -39,7 +39,8 @@ library_path = os.path.join(_HERE, "liblighthouse.so")
 EXPORTED = [
     "lh_check", "lh_level_rows", "lh_level_offset", "lh_pyramid_rows", "lh_subseq_len",
     "lh_workspace_bytes", "lh_status_str", "lh_last_error", "lh_pyramid_pool", "lh_score",
-    "lh_pool_score", "lh_select_topk", "lh_gather", "lh_sdpa_fwd", "lh_sdpa_bwd", "lh_scatter", "lh_scatter_bwd",
+    "lh_pool_score", "lh_select_topk", "lh_gather", "lh_sdpa_fwd", "lh_sdpa_bwd", "lh_sdpa_bwd_noalloc",
+    "lh_scatter", "lh_scatter_bwd",
     "lh_gather_bwd", "lh_attention_fwd", "lh_attention_bwd", "lh_sdpa_fwd_indexed", "lh_sdpa_bwd_indexed",
     "lh_attention_fwd_indexed", "lh_attention_bwd_indexed",
 ]
@@ -96,6 +97,7 @@ def _load():
         "lh_gather": (i32, [PR, P, P, P, P, P, P, P, P, P, P, P]),
         "lh_sdpa_fwd": (i32, [PR, P, P, P, P, P, P]),
         "lh_sdpa_bwd": (i32, [PR, P, P, P, P, P, P, P, P, P, P, sz, P]),
+        "lh_sdpa_bwd_noalloc": (i32, [PR, P, P, P, P, P, P, P, P, P, P]),
         "lh_scatter": (i32, [PR, P, P, P, P]),
         "lh_scatter_bwd": (i32, [PR, P, P, P, P]),
         "lh_gather_bwd": (i32, [PR, P, P, P, P, P, P, P, P]),
@@ -273,6 +275,14 @@ def lh_sdpa_bwd(pr, qs, ks, vs, os_, lse, dos, dqs, dks, dvs, ws, ws_bytes=None,
           (ws, "ws", "ws"))
     _call("lh_sdpa_bwd", ctypes.byref(pr), _p(qs), _p(ks), _p(vs), _p(os_), _p(lse), _p(dos), _p(dqs),
           _p(dks), _p(dvs), _p(ws), _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream))
+
+
+def lh_sdpa_bwd_noalloc(pr, qs, ks, vs, os_, lse, dos, dqs, dks, dvs, stream=None):
+    """lh_sdpa_bwd with its workspace in the library's static device scratch (allocates nothing)."""
+    _need("lh_sdpa_bwd_noalloc", pr, (qs, "qs", "qs"), (ks, "ks", "kvs"), (vs, "vs", "kvs"), (os_, "os", "qs"),
+          (lse, "lse", "lse"), (dos, "dos", "qs"), (dqs, "dqs", "qs"), (dks, "dks", "kvs"), (dvs, "dvs", "kvs"))
+    _call("lh_sdpa_bwd_noalloc", ctypes.byref(pr), _p(qs), _p(ks), _p(vs), _p(os_), _p(lse), _p(dos), _p(dqs),
+          _p(dks), _p(dvs), _stream(stream))
 
 
 def lh_scatter(pr, os_, slot, o, stream=None):

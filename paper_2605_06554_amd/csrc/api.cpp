@@ -360,6 +360,31 @@ lh_status lh_sdpa_bwd(const lh_problem* pr, const void* qs, const void* ks, cons
                     "lh_sdpa_bwd");
 }
 
+lh_status lh_sdpa_bwd_noalloc(const lh_problem* pr, const void* qs, const void* ks, const void* vs,
+                              const void* os, const float* lse, const void* dos, void* dqs, void* dks,
+                              void* dvs, void* stream) {
+  LhShape s;
+  LH_TRY(make_shape(pr, &s));
+  LH_TRY(need_ptr(qs, "qs"));
+  LH_TRY(need_ptr(ks, "ks"));
+  LH_TRY(need_ptr(vs, "vs"));
+  LH_TRY(need_ptr(os, "os"));
+  LH_TRY(need_ptr(lse, "lse"));
+  LH_TRY(need_ptr(dos, "dos"));
+  LH_TRY(need_ptr(dqs, "dqs"));
+  LH_TRY(need_ptr(dks, "dks"));
+  LH_TRY(need_ptr(dvs, "dvs"));
+  const size_t need = (size_t)s.B * s.Hq * s.S * sizeof(float);
+  if (need > lh_sdpa_scratch_bytes())
+    return fail(LH_E_WORKSPACE, "lh_sdpa_bwd_noalloc: Delta needs %zu bytes, the static scratch holds %zu (B*Hq*S <= %zu)",
+                need, lh_sdpa_scratch_bytes(), lh_sdpa_scratch_bytes() / sizeof(float));
+  float* delta = nullptr;
+  LH_TRY(hip_status(lh_sdpa_scratch(&delta), "lh_sdpa_bwd_noalloc: scratch address"));
+  g_err[0] = 0;
+  return hip_status(lh_launch_sdpa_bwd(s, qs, ks, vs, os, lse, dos, dqs, dks, dvs, delta, (hipStream_t)stream),
+                    "lh_sdpa_bwd_noalloc");
+}
+
 lh_status lh_scatter(const lh_problem* pr, const void* os, const int32_t* slot, void* o, void* stream) {
   LhShape s;
   LH_TRY(make_shape(pr, &s));

@@ -2,6 +2,8 @@
 // Eq. sdpa): dispatch, the Delta = rowsum(dO * O) kernel of the backward, and the fp32 path
 // (plain per-row kernels, a thread per row, used for fp32 problems). The bf16 MFMA kernels are
 // in k_sdpa_mfma.hip.
+#include <mutex>
+
 #include "lh_common.h"
 
 hipError_t lh_launch_sdpa_fwd_bf16(const LhShape& s, const void* qs, const void* ks, const void* vs, void* os,
@@ -274,4 +276,35 @@ hipError_t lh_launch_sdpa_bwd(const LhShape& s, const void* qs, const void* ks, 
                        s.Hq, s.Hs, s.Gq);
   }
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ scratch of lh_sdpa_bwd_noalloc
+// Delta of the backward (B * Hq * S floats) for callers that cannot allocate: a file-scope
+// device array, one copy per GPU, held until the process ends. Its address on the current
+// device is looked up once per device with hipGetSymbolAddress; host code never passes the
+// array's name itself to a kernel. sdpa_delta overwrites every element a call reads, so
+// nothing needs clearing between calls; calls that overlap on one GPU share the array and race.
+static constexpr size_t kSdpaScratchBytes = (size_t)16 << 20;
+static constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kSdpaScratchBytes];
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices] = {};
+
+size_t lh_sdpa_scratch_bytes() { return kSdpaScratchBytes; }
+
+hipError_t lh_sdpa_scratch(float** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = reinterpret_cast<float*>(g_scratch_ptr[dev]);
+  return hipSuccess;
 }

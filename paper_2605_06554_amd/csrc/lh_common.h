@@ -170,3 +170,7 @@ hipError_t lh_launch_sdpa_bwd_indexed(const LhShape& s, const void* q, const voi
                                       const int32_t* idx, const void* os, const float* lse,
                                       const void* dos, void* dqs, void* dks, void* dvs, float* delta,
                                       hipStream_t st);
+// Static device scratch of lh_sdpa_bwd_noalloc (k_sdpa.hip): its size in bytes, and its address
+// on the current device (looked up once per device).
+size_t lh_sdpa_scratch_bytes();
+hipError_t lh_sdpa_scratch(float** out);

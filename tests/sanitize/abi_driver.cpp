@@ -67,6 +67,11 @@ static const Entry kEntries[] = {
        return lh_sdpa_bwd(pr, P(0), P(1), P(2), P(3), (float*)P(4), P(5), P(6), P(7), P(8), ws, n, nullptr);
      },
      false, -1, -1},
+    {"lh_sdpa_bwd_noalloc", 9, -1,
+     [](const lh_problem* pr, void** v, void*, size_t) {
+       return lh_sdpa_bwd_noalloc(pr, P(0), P(1), P(2), P(3), (float*)P(4), P(5), P(6), P(7), P(8), nullptr);
+     },
+     false, -1, -1},
     {"lh_scatter", 3, -1,
      [](const lh_problem* pr, void** v, void*, size_t) { return lh_scatter(pr, P(0), (int32_t*)P(1), P(2), nullptr); },
      false, -1, -1},
@@ -212,6 +217,15 @@ int main() {
     const int before = g_launches;
     for (const Entry& e : kEntries) EXPECT(e.call(&pr, v.data(), fake(0), (size_t)1 << 40) == st, "%s on invalid %d", e.name, i);
     EXPECT(g_launches == before, "launch on an invalid problem");
+  }
+  {  // the static scratch of lh_sdpa_bwd_noalloc holds B * Hq * S <= 4,194,304 floats
+    const lh_problem big = mk(4, 65536, 32, 32, 128, 4, 4, 4096, LH_BF16, 0);
+    std::vector<void*> v(16);
+    for (int i = 0; i < 16; ++i) v[i] = fake(i + 1);
+    const int before = g_launches;
+    EXPECT(lh_sdpa_bwd_noalloc(&big, v[0], v[1], v[2], v[3], (float*)v[4], v[5], v[6], v[7], v[8], nullptr) ==
+               LH_E_WORKSPACE, "noalloc: oversize problem accepted");
+    EXPECT(g_launches == before, "noalloc: launched an oversize problem");
   }
   EXPECT(lh_check(nullptr) == LH_E_NULL, "NULL problem");
   for (int c = 1; c >= -8; --c) EXPECT(lh_status_str((lh_status)c) != nullptr, "status string");

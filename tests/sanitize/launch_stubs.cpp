@@ -40,3 +40,10 @@ hipError_t lh_launch_sdpa_fwd_indexed(const LhShape& s, const void*, const void*
 hipError_t lh_launch_sdpa_bwd_indexed(const LhShape& s, const void*, const void*, const void*, const void*,
                                       const void*, const void*, const int32_t*, const void*, const float*,
                                       const void*, void*, void*, void*, float*, hipStream_t) { return ok(s); }
+
+// the static scratch of lh_sdpa_bwd_noalloc: a fake device address, never dereferenced here
+size_t lh_sdpa_scratch_bytes() { return (size_t)16 << 20; }
+hipError_t lh_sdpa_scratch(float** out) {
+  *out = reinterpret_cast<float*>((uintptr_t)0x7f000000ull);
+  return hipSuccess;
+}
