@@ -305,6 +305,41 @@ def ceilings():
     return out
 
 
+def dq_atomics_probe():
+    """The dQ accumulation a single-pass SDPA backward would add to the dK/dV kernel at c4
+    (libceiling.so lh_probe_dq_sweep: its block order and query sweep, 64 x 128 fp32 tiles in the
+    MFMA output layout), as relaxed device-scope float atomics and, for comparison, as plain
+    stores of the same tiles, alone and beside 80 MFMAs per wave and tile (the 5 GEMMs of a
+    single pass)."""
+    import ctypes
+
+    import paper_2605_06554_amd as lh
+
+    lib = ctypes.CDLL(os.path.join(os.path.dirname(lh.library_path), "libceiling.so"))
+    lib.lh_probe_dq_sweep.restype = ctypes.c_int64
+    lib.lh_probe_dq_sweep.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_int32, ctypes.c_void_p]
+    S, heads = 54272, 32
+    stream = torch.cuda.current_stream()
+    dq = torch.zeros(heads * S * 128, dtype=torch.float32, device="cuda")
+    out = {}
+    for mode, name in ((0, "atomics"), (1, "stores")):
+        for nmfma in (0, 80):
+            nbytes = [0]
+
+            def run():
+                nbytes[0] = lib.lh_probe_dq_sweep(dq.data_ptr(), S, heads, mode, nmfma,
+                                                  ctypes.c_void_p(stream.cuda_stream))
+                if nbytes[0] < 0:
+                    raise RuntimeError("lh_probe_dq_sweep failed")
+
+            print(f"[probe] dq sweep: {name}, {nmfma} MFMA per wave and tile", file=sys.stderr, flush=True)
+            ms = _median_ms(run, 3, stream)
+            out[f"{name}_mfma{nmfma}"] = dict(ms=round(ms, 2), payload_gb=round(nbytes[0] / 1e9, 2),
+                                             tb_per_s=round(nbytes[0] / (ms * 1e-3) / 1e12, 3))
+    return out
+
+
 def host_cpu():
     model = ""
     try:
@@ -387,6 +422,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--stage-reps", type=int, default=10, help="timed calls per stage (median)")
     ap.add_argument("--no-ceilings", action="store_true", help="skip the achievable-rate probes")
+    ap.add_argument("--dq-atomics-probe", action="store_true",
+                    help="time the dQ atomics a single-pass SDPA backward would need at c4, then exit")
     ap.add_argument("--config", default="c4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=16384,
@@ -402,6 +439,10 @@ def main():
               "over several GPUs (by KV-head group) is not built, so --gpus must be 1.",
               file=sys.stderr)
         raise SystemExit(2)
+    if args.dq_atomics_probe:
+        torch.cuda.set_device(0)
+        print(json.dumps(dict(dq_atomics_probe=dq_atomics_probe())), flush=True)
+        return
     cfg = {**workloads.CONFIGS, **workloads.SHARD_CONFIGS}[args.config]
     if args.gqa_shared:
         cfg = workloads.scaled(cfg, name=cfg.name + "-gqa-shared", flags=cfg.flags | 4)

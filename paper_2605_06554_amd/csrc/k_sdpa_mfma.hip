@@ -583,6 +583,12 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
   }
   const float lse2 = myq < S ? LSE[bh * S + myq] * kLog2e : INFINITY;
   const float dlt = myq < S ? DELTA[bh * S + myq] : 0.0f;
+  // every element of a lane's dP^T accumulator belongs to the lane's query row: the chain starts
+  // from -Delta (a separate source operand of its first MFMA), so it ends as dP - Delta and no
+  // subtraction is needed
+  f32x16 ndlt;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) ndlt[i] = -dlt;
 #pragma unroll
   for (int t = 0; t < QNS - 1; ++t) load_kv(t, t * BK);
   f32x16 dqacc[D / 32];
@@ -604,12 +610,16 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
     const bf16_t* Vt = Vs[SL];
 #pragma unroll
     for (int kb = 0; kb < BK / 32; ++kb) {
-      f32x16 sacc = f32x16{}, pacc = f32x16{};
+      f32x16 sacc = f32x16{};
+      f32x16 pacc = mfma32(row8(Vt, kb * 32 * RB + lo.row[0]), doreg[0], ndlt);
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) {
         sacc = mfma32(row8(Kt, kb * 32 * RB + lo.row[kk]), qreg[kk], sacc);
-        pacc = mfma32(row8(Vt, kb * 32 * RB + lo.row[kk]), doreg[kk], pacc);
+        if (kk > 0) pacc = mfma32(row8(Vt, kb * 32 * RB + lo.row[kk]), doreg[kk], pacc);
       }
+      // causal mask: element i holds key k0 + 32 kb + 4h + c_i, c_i = 8 (i / 4) + i % 4, which is
+      // in the future of the lane's query exactly when c_i > tm
+      const int tm = myq - k0 - kb * 32 - 4 * h;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         float f[8];
@@ -617,8 +627,8 @@ sdpa_bwd_dq_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, con
         for (int t = 0; t < 8; ++t) {
           const int i = 8 * u + t;
           float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[i], sl2, -lse2));
-          if (MASK && k0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3) > myq) pv = 0.0f;
-          f[t] = pv * (pacc[i] - dlt);
+          if (MASK && 8 * (i >> 2) + (i & 3) > tm) pv = 0.0f;
+          f[t] = pv * pacc[i];
         }
         const bf16x8 db = cvt8(f);
 #pragma unroll
