@@ -22,7 +22,8 @@ lh_status fail(lh_status s, const char* fmt, ...) {
 }
 
 constexpr int kMaxLevels = 8;       // kernels are instantiated for L = 1..8
-constexpr int64_t kMaxSelect = 32768;  // candidates of one level ranked in LDS (128 KB of keys)
+constexpr int64_t kSelLdsKeys = 32768;        // a level up to this many candidates ranks in LDS
+constexpr int64_t kMaxSelect = (int64_t)1 << 26;  // beyond: keys in the workspace (ids < 2^30)
 
 lh_status make_shape(const lh_problem* pr, LhShape* s) {
   if (!pr) return fail(LH_E_NULL, "problem is NULL");
@@ -92,6 +93,14 @@ lh_status make_shape(const lh_problem* pr, LhShape* s) {
 size_t esize(const LhShape& s) { return s.dtype == LH_BF16 ? 2 : 4; }
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Selection workspace: the candidate lists [B, Hs, Scand] int32, then, when a level ranks more
+// candidates than fit in LDS, one row of maxsel uint32 keys per selection.
+size_t sel_bytes(const LhShape& s) {
+  size_t b = (size_t)s.B * s.Hs * s.Scand * 4;
+  if (s.maxsel > kSelLdsKeys) b += (size_t)s.B * s.Hs * s.maxsel * 4;
+  return b;
+}
+
 // Workspace layouts (offsets in bytes, each segment 256-byte aligned).
 struct FwdWs {
   size_t qpyr, kpyr, vpyr, s_qk, s_kq, sel, total;
@@ -105,7 +114,7 @@ FwdWs fwd_ws(const LhShape& s) {
   w.vpyr = o, o += align256((size_t)s.B * s.R * s.Hkv * s.D * es);
   w.s_qk = o, o += align256((size_t)s.B * s.Hq * s.Ptot * 4);
   w.s_kq = o, o += align256((size_t)s.B * s.Hkv * s.Ptot * 4);
-  w.sel = o, o += align256((size_t)s.B * s.Hs * s.Scand * 4);
+  w.sel = o, o += align256(sel_bytes(s));
   w.total = o;
   return w;
 }
@@ -128,7 +137,7 @@ BwdWs bwd_ws(const LhShape& s) {
 
 size_t ws_bytes(const LhShape& s, int op) {
   switch (op) {
-    case LH_OP_SELECT: return align256((size_t)s.B * s.Hs * s.Scand * 4);
+    case LH_OP_SELECT: return align256(sel_bytes(s));
     case LH_OP_SDPA_BWD: return align256((size_t)s.B * s.Hq * s.S * 4);
     case LH_OP_ATTENTION_FWD: return fwd_ws(s).total;
     case LH_OP_ATTENTION_BWD: return bwd_ws(s).total;

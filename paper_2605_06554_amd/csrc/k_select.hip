@@ -2,7 +2,8 @@
 // ordering of the selected entries (Sec. 3.5, mask paragraph).
 //
 // select_kernel: one workgroup of 1024 threads per (b, selection head). Per level l = L-1 .. 1
-// it ranks the level's candidates (a sorted list of level-local indices) by the 32-bit key
+// it ranks the level's candidates (a sorted list of level-local indices; their keys in LDS, or in
+// a global workspace row when a level has more than 32,768 candidates) by the 32-bit key
 // bits(max(s_QK, s_KQ)) -- non-negative floats, so the bit pattern orders them -- and finds the
 // exact threshold of the k best by an MSB-first radix select (8-bit digits below the bits all
 // keys share, LDS histograms with integer atomics; one wave reads each digit off the histogram
@@ -28,10 +29,17 @@ constexpr int kSelThreads = 1024;
 constexpr int64_t kStratChunk = 2048;
 constexpr int kSelWaves = kSelThreads / 64;
 
+// Levels of at most this many candidates keep their keys in LDS (128 KB); larger levels keep
+// them in a global workspace region of their own (one row of maxsel keys per selection), which
+// the radix passes stream through L2.
+constexpr int64_t kSelLdsKeys = 32768;
+
 struct SelArgs {
   const float* s_qk;
   const float* s_kq;
   int32_t* ws;  // [B, Hq, Scand] candidate lists, level-major
+  uint32_t* gkeys;  // [B, Hs, maxsel] keys when maxsel > kSelLdsKeys, else null
+  int64_t maxsel;
   int64_t Ptot, Scand;
   int32_t Hq, Hkv, G, L, p;
   int32_t Hs, Gq;  // selection heads; query heads whose scores one selection ranks
@@ -74,11 +82,14 @@ __device__ __forceinline__ void select_bin(const int* hist, uint32_t* sel_state,
   }
 }
 
+// GK: the level's keys live in the global rows a.gkeys (levels above kSelLdsKeys candidates)
+// instead of LDS; the algorithm is the same.
+template <bool GK>
 __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
-  extern __shared__ uint32_t keys[];  // candidate keys of the current level
+  extern __shared__ uint32_t keys_lds[];  // candidate keys of the current level
   __shared__ __align__(16) int hist[256];
   __shared__ uint32_t sel_state[2];  // prefix, remaining
-  __shared__ int wave_cnt[kSelWaves];  // (greater << 16) | equal counts of each wave's candidates
+  __shared__ int wave_gt[kSelWaves], wave_eq[kSelWaves];  // counts of each wave's candidates
   __shared__ uint32_t key_and[kSelWaves], key_or[kSelWaves];  // per-wave AND / OR of the keys
 
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -90,6 +101,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
   const float* sq = a.s_qk + (b * a.Hq + (int64_t)hs * a.Gq) * a.Ptot;
   const float* sk = a.s_kq + (b * a.Hkv + g) * a.Ptot;
   int32_t* C = a.ws + (int64_t)bs * a.Scand;
+  uint32_t* keys = GK ? a.gkeys + (int64_t)bs * a.maxsel : keys_lds;
   const int L = a.L, p = a.p;
 
   // top level: every entry is a candidate
@@ -226,13 +238,16 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
           if (u < c1) keys[u] = (uint32_t)ids[j] | (gt ? 0x80000000u : 0u) | (eq ? 0x40000000u : 0u);
         }
       }
-      if (lane == 0) wave_cnt[wv] = (gt_w << 16) | eq_w;
+      if (lane == 0) {
+        wave_gt[wv] = gt_w;
+        wave_eq[wv] = eq_w;
+      }
+      if (GK) __threadfence_block();  // the keys rewritten above are read by the same wave below
       __syncthreads();
       int gt_rank = 0, eq_rank = 0;  // candidates of the earlier waves
       for (int i = 0; i < wv; ++i) {
-        const int x = wave_cnt[i];
-        gt_rank += x >> 16;
-        eq_rank += x & 0xffff;
+        gt_rank += wave_gt[i];
+        eq_rank += wave_eq[i];
       }
       const uint64_t below = (1ull << lane) - 1ull;
       for (int64_t base = c0; base < c1; base += 64) {
@@ -406,8 +421,14 @@ hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_
   for (int l = 0; l < 17; ++l) a.off[l] = s.off[l], a.coff[l] = s.coff[l];
   for (int l = 0; l < 16; ++l) a.cand[l] = s.cand[l], a.npar[l] = s.npar[l];
   a.stratified = (s.flags & LH_FLAG_STRATIFIED) ? 1 : 0;
-  const size_t shm = (size_t)(s.maxsel > 0 ? s.maxsel : 1) * sizeof(uint32_t);
-  hipLaunchKernelGGL(select_kernel, dim3((unsigned)BH), dim3(kSelThreads), shm, st, a);
+  a.maxsel = s.maxsel;
+  a.gkeys = s.maxsel > kSelLdsKeys ? reinterpret_cast<uint32_t*>(ws + BH * s.Scand) : nullptr;
+  if (a.gkeys) {
+    hipLaunchKernelGGL(select_kernel<true>, dim3((unsigned)BH), dim3(kSelThreads), 0, st, a);
+  } else {
+    const size_t shm = (size_t)(s.maxsel > 0 ? s.maxsel : 1) * sizeof(uint32_t);
+    hipLaunchKernelGGL(select_kernel<false>, dim3((unsigned)BH), dim3(kSelThreads), shm, st, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
 

@@ -48,7 +48,8 @@ def _pr(**kw):
     (dict(flags=8), -3),
     (dict(N=0), -2),
     (dict(L=1, p=0), 0),                # p is irrelevant with one level
-    (dict(N=2 ** 20, L=2, k=1000), -3),  # one level would rank 262144 candidates
+    (dict(N=2 ** 20, L=2, k=1000), 0),   # a level of 262144 candidates ranks with its keys in the workspace
+    (dict(N=2 ** 28, p=2, L=2, k=1), -3),  # 2^27 candidates at one level: beyond the 2^26 supported
     (dict(scale=-0.125), -3),           # a negative softmax scale is refused
     (dict(scale=float("nan")), -3),
 ])

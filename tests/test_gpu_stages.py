@@ -109,7 +109,11 @@ def test_select_fig2_toy():
                                            (2187, 3, 3, 50, 1), (16384, 4, 5, 4096, 0), (65536, 4, 3, 8192, 0),
                                            # stratified: several chunks of 2048 candidates per level
                                            (65536, 4, 3, 8192, 2), (65536, 4, 2, 3000, 2), (8192, 2, 3, 1500, 3),
-                                           (6561, 3, 3, 900, 2)])
+                                           (6561, 3, 3, 900, 2),
+                                           # levels of 40,000 and 131,072 candidates: keys in the
+                                           # workspace instead of LDS
+                                           (262144, 4, 3, 10000, 0), (262144, 4, 3, 10000, 2),
+                                           (262144, 2, 2, 50000, 1)])
 def test_select_random_scores(N, p, L, k, flags, ties, rng):
     Hq, Hkv = 4, 2
     print(f"[stage select] N={N} p={p} L={L} k={k} flags={flags} ties={ties}", flush=True)
@@ -131,7 +135,8 @@ def test_select_random_scores(N, p, L, k, flags, ties, rng):
 
 
 @pytest.mark.parametrize("kind", ["constant", "low_bits", "wide", "zeros"])
-@pytest.mark.parametrize("N,p,L,k,flags", [(16384, 4, 5, 4096, 0), (65536, 4, 3, 8192, 2), (4096, 4, 4, 100, 1)])
+@pytest.mark.parametrize("N,p,L,k,flags", [(16384, 4, 5, 4096, 0), (65536, 4, 3, 8192, 2), (4096, 4, 4, 100, 1),
+                                           (262144, 4, 3, 10000, 0)])
 def test_select_key_bit_patterns(kind, N, p, L, k, flags, rng):
     # Score patterns that drive the radix select's digit choice to its edges: every key equal
     # (no digit pass at all), keys that differ only in the lowest mantissa bits (one short
@@ -161,6 +166,35 @@ def test_select_key_bit_patterns(kind, N, p, L, k, flags, rng):
             ri, rs = oracle.select(h, sq[b, hq], sk[b, hq // 2])
             check_equal(f"idx[{b},{hq}]", idx[b, hq], ri)
             check_equal(f"slot[{b},{hq}]", slot[b, hq], rs)
+
+
+def test_select_large_levels_from_scores():
+    """The c5 shape (N = 1,048,576, p = 4, L = 6) with k = 16,384: levels 2 and 1 rank 65,536
+    candidates each, beyond the LDS key buffer. Scores from lh_pool_score on device inputs, then
+    lh_select_topk; scores, idx and slot against the oracle, bit for bit."""
+    c = workloads.scaled(workloads.CONFIGS["c5"], Hq=2, Hkv=2, k=16384, name="c5-k16384")
+    print("[stage select] c5 shape with k = 16384", flush=True)
+    pr = _problem(c)
+    S, Ptot = lh.lh_subseq_len(pr), lh.lh_pyramid_rows(pr)
+    assert S == 1024 + 4096 + 16384 + 3 * 65536
+    inp = workloads.make_inputs(c, device=DEV, with_grad=False)
+    q, k, v = inp["q"], inp["k"], inp["v"]
+    R = Ptot - c.N
+    qp = torch.empty(c.B, R, c.Hq, c.D, dtype=q.dtype, device=DEV)
+    kp, vp = torch.empty(c.B, R, c.Hkv, c.D, dtype=q.dtype, device=DEV), torch.empty(c.B, R, c.Hkv, c.D, dtype=q.dtype, device=DEV)
+    sqk = torch.empty(c.B, c.Hq, Ptot, dtype=torch.float32, device=DEV)
+    skq = torch.empty(c.B, c.Hkv, Ptot, dtype=torch.float32, device=DEV)
+    lh.lh_pool_score(pr, q, k, v, qp, kp, vp, sqk, skq)
+    idx, slot = _run_select(pr, sqk, skq)
+    h = oracle.Head(c.N, c.D, c.p, c.L, c.k, oracle.BF16)
+    for hq in range(c.Hq):
+        s_qk = oracle.scores(h, np.ascontiguousarray(q[0, :, hq].double().cpu().numpy()))
+        s_kq = oracle.scores(h, np.ascontiguousarray(k[0, :, hq].double().cpu().numpy()))
+        check_equal(f"s_qk[{hq}]", sqk[0, hq], s_qk)
+        check_equal(f"s_kq[{hq}]", skq[0, hq], s_kq)
+        ri, rs = oracle.select(h, s_qk, s_kq)
+        check_equal(f"idx[{hq}]", idx[0, hq], ri)
+        check_equal(f"slot[{hq}]", slot[0, hq], rs)
 
 
 def _layer_oracle(c, inp):
