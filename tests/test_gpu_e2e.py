@@ -26,7 +26,8 @@ def _run(c, inp):
     return pr, st, (dq, dk, dv)
 
 
-@pytest.mark.parametrize("name", ["c1", "t_gqa", "t_f32", "t_p3", "t_l1", "t_k0", "t_strat", "t_l2", "t_l2g", "t_p3g", "t_p5g", "t_l8", "t_g3"])
+@pytest.mark.parametrize("name", ["c1", "t_gqa", "t_f32", "t_p3", "t_l1", "t_k0", "t_strat", "t_l2", "t_l2g", "t_p3g", "t_p5g", "t_l8", "t_g3",
+                                  "t_grp4", "t_grp_tail", "t_grp_f32", "t_grp_wide"])
 def test_layer_matches_oracle(name):
     c = _cfg(name)
     print(f"[e2e] {name}", flush=True)

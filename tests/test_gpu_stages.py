@@ -34,7 +34,8 @@ def _odt(c):
     return oracle.BF16 if c.dtype == "bf16" else oracle.F32
 
 
-STAGE_CFGS = ["c1", "t_gqa", "t_f32", "t_p3", "t_k0", "t_l2", "t_l2g", "t_p3g", "t_p5g", "t_l8", "t_g3"]
+STAGE_CFGS = ["c1", "t_gqa", "t_f32", "t_p3", "t_k0", "t_l2", "t_l2g", "t_p3g", "t_p5g", "t_l8", "t_g3",
+              "t_grp4", "t_grp_tail", "t_grp_f32", "t_grp_wide"]
 
 
 @pytest.mark.parametrize("name", STAGE_CFGS + ["t_l1"])
@@ -241,7 +242,8 @@ def test_gather_sdpa_scatter_stages(name):
             check_close(f"os[{b},{hq}]", os_[b, hq], f["os"][b, hq], c.dtype, fl)
             check_close(f"lse[{b},{hq}]", lse[b, hq], f["lse"][b, hq], "fp32")
     # scatter of the oracle's own sub-sequence output (rounded to the dtype) isolates the scatter
-    os_ref = torch.from_numpy(f["os"]).to(dt).to(DEV)
+    os_ref_h = torch.from_numpy(f["os"]).to(dt)
+    os_ref = os_ref_h.to(DEV)
     o = torch.empty_like(q)
     lh.lh_scatter(pr, os_ref, slot, o)
     torch.cuda.synchronize()
@@ -257,11 +259,16 @@ def test_gather_sdpa_scatter_stages(name):
         for hq in range(c.Hq):
             check_close(f"dos[{b},{hq}]", dos[b, hq], g["dos"][b, hq], c.dtype,
                         rounding_floor(g["dos"][b, hq]) if bf else None)
-    # SDPA backward on the oracle's inputs (os/lse from the GPU forward)
+    # SDPA backward on the oracle's inputs: its os rounded to the dtype, its lse, and its dos
+    # rounded to the dtype. The floor emulation takes the same rounded os: with planted key
+    # spikes, dQ~ depends on the rounding of os through Delta = rowsum(dO~ * O~) amplified by
+    # the spiked keys, so the GPU forward's own os (another valid rounding) would make the
+    # backward's error a different sample from the emulated one.
     dqs, dks, dvs = (torch.empty(c.B, c.Hq, S, c.D, dtype=dt, device=DEV) for _ in range(3))
     dos_ref = torch.from_numpy(g["dos"]).to(dt).to(DEV)
+    lse_ref = torch.from_numpy(np.asarray(f["lse"], np.float32)).to(DEV)
     ws = lh.workspace(pr, lh.LH_OP_SDPA_BWD)
-    lh.lh_sdpa_bwd(pr, qs, ks, vs, os_, lse, dos_ref, dqs, dks, dvs, ws)
+    lh.lh_sdpa_bwd(pr, qs, ks, vs, os_ref, lse_ref, dos_ref, dqs, dks, dvs, ws)
     torch.cuda.synchronize()
     for b in range(c.B):
         for hq in range(c.Hq):
@@ -269,7 +276,8 @@ def test_gather_sdpa_scatter_stages(name):
             rq, rk, rv = oracle.sdpa_bwd(*args, f["os"][b, hq], f["lse"][b, hq], to64(dos_ref[b, hq]), sc)
             fq = fk = fv = None
             if bf:
-                eq, ek, ev = bf16_floor.sdpa_bwd(*args, os_emu[b, hq], f["lse"][b, hq], to64(dos_ref[b, hq]), sc)
+                eq, ek, ev = bf16_floor.sdpa_bwd(*args, os_ref_h[b, hq].double().numpy(), f["lse"][b, hq],
+                                                 to64(dos_ref[b, hq]), sc)
                 fq = emulated_floor(eq, rq)
                 fk = emulated_floor(bf16_floor.round_bf16(ek), rk)
                 fv = emulated_floor(bf16_floor.round_bf16(ev), rv)

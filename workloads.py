@@ -94,6 +94,14 @@ TEST_CONFIGS = {
     "t_l8": Config("t_l8", 1, 2048, 2, 1, 64, 2, 8, 12, "bf16", 2015),
     # p = 2, L = 5, N = 112: Ptot = 217 (odd), three query heads per KV head
     "t_g3": Config("t_g3", 1, 112, 3, 1, 64, 2, 5, 5, "bf16", 2008),
+    # dK / dV gather adjoint over runs of 8 positions with a whole wave or more per run (p = 4,
+    # 2 or 4 query heads per KV head, the unpacked launch of the c4 layer): G = 4 with spiked
+    # keys (Ptot = 5440); a partial last run (N = 4 * 257); fp32; two workgroups per run
+    # (32 KV heads, 512 threads of work per run)
+    "t_grp4": Config("t_grp4", 1, 4096, 16, 4, 128, 4, 4, 128, "bf16", 2016, "spikes", 0.01),
+    "t_grp_tail": Config("t_grp_tail", 2, 1028, 8, 4, 128, 4, 2, 64, "bf16", 2017),
+    "t_grp_f32": Config("t_grp_f32", 2, 1024, 8, 4, 64, 4, 3, 32, "fp32", 2018),
+    "t_grp_wide": Config("t_grp_wide", 1, 256, 64, 32, 128, 4, 3, 8, "bf16", 2019),
     # one selection per KV group (flag bit 2): G = 2, p = 4; G = 3, p = 2; G = 4 in fp32
     "t_gqs": Config("t_gqs", 1, 4096, 4, 2, 128, 4, 4, 256, "bf16", 2009, "spikes", 0.01, flags=4),
     "t_gqs3": Config("t_gqs3", 1, 2048, 6, 2, 64, 2, 5, 40, "bf16", 2010, flags=4),
