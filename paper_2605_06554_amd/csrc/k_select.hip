@@ -15,11 +15,12 @@
 // consecutive candidates, each keeping its proportional share of the k parents.
 // No floating-point atomics: the result is bitwise deterministic.
 //
-// order_kernel: one thread per candidate. Emitted entries are sorted by
-// key = e * L + (L - 1 - l), e = (i + 1) p^l - 1 (window end, coarser level first on ties).
-// Each level's list is sorted by i, hence by key, so an entry's rank is the sum over levels of
-// a binary search (merge by rank, no general sort); the searches of the levels advance in
-// lockstep. It writes idx[rank] and slot[id] = rank.
+// order_kernel: emitted entries are sorted by key = e * L + (L - 1 - l), e = (i + 1) p^l - 1
+// (window end, coarser level first on ties). A workgroup owns a range of window ends: its
+// entries are a contiguous part of each level's sorted list, the emitted entries before the
+// range are counted by lower bounds in those lists, and a scan over the range's (end, level)
+// flags orders the rest. It writes idx[rank], and slot for every pyramid entry (-1 for those
+// not gathered), so slot needs no separate fill.
 #include "lh_common.h"
 
 namespace lh {
@@ -275,19 +276,20 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
 
 struct OrdArgs {
   const int32_t* ws;
-  int32_t* idx;   // [B, Hq, S]
-  int32_t* slot;  // [B, Hq, Ptot]
-  int64_t Ptot, Scand, S;
-  int32_t L, p, replace;
-  int64_t off[17];
-  int64_t pw[16];
-  int64_t cand[16];
-  int64_t coff[17];
-  int64_t nrows[16];  // N / p^l
+  int32_t* idx;   // [B, Hs, S]
+  int32_t* slot;  // [B, Hs, Ptot]
+  int64_t Scand;
+  int32_t Ptot, S, N, L, p, replace;
+  int32_t lsh[16];   // l log2(p) when p is a power of two, else -1
+  int32_t pw[16];    // p^l
+  int32_t off[17];   // flattened id of entry (l, 0)
+  int32_t cand[16];  // candidates of level l
+  int32_t coff[17];  // offset of level l's list in a selection's workspace row
 };
 
-__device__ __forceinline__ int64_t order_key(int64_t i, int l, const OrdArgs& a) {
-  return ((i + 1) * a.pw[l] - 1) * a.L + (a.L - 1 - l);
+// floor(x / p^l) for 0 <= x < 2^31
+__device__ __forceinline__ int32_t div_pw(int32_t x, int l, const OrdArgs& a) {
+  return a.lsh[l] >= 0 ? x >> a.lsh[l] : (int32_t)((uint32_t)x / (uint32_t)a.pw[l]);
 }
 
 // number of entries of the sorted int list c[0, n) below value x
@@ -301,93 +303,168 @@ __device__ __forceinline__ int64_t lower_bound_val(const int32_t* c, int64_t n, 
   return lo;
 }
 
+// Window ends per workgroup of order_kernel (a multiple of 8192 / L for every L, so that the
+// range's flag words split evenly over 256 threads).
+constexpr int kOrdE = 8192;
 
-// Lower bounds in the sorted lists C + coff[l], l < NL: lo[l] ends as the number of entries v
-// of list l with below(l, v) true (below is monotone along each list). The lists advance
-// together: every step loads one probe of each list still open before comparing any.
-template <int NL, typename F>
-__device__ __forceinline__ void lockstep_search(int32_t* lo, int32_t* hi, const OrdArgs& a, F below) {
-  const int32_t* C = a.ws + (int64_t)blockIdx.y * a.Scand;
-  for (;;) {
-    int32_t v[NL];
-    bool open = false;
-#pragma unroll
-    for (int l = 0; l < NL; ++l) {
-      v[l] = 0;
-      if (lo[l] < hi[l]) {
-        v[l] = C[a.coff[l] + ((lo[l] + hi[l]) >> 1)];
-        open = true;
-      }
-    }
-    if (!__builtin_amdgcn_ballot_w64(open)) break;
-#pragma unroll
-    for (int l = 0; l < NL; ++l) {
-      if (lo[l] < hi[l]) {
-        const int32_t mid = (lo[l] + hi[l]) >> 1;
-        if (below(l, v[l])) lo[l] = mid + 1;
-        else hi[l] = mid;
-      }
-    }
-  }
-}
-
+// order_kernel: workgroup x of a selection owns the window ends e in [e0, e1), e0 = x kOrdE:
+// the level-l entries i in [floor(e0 / p^l), floor(e1 / p^l)), a contiguous part of each level's
+// sorted candidate list. Ranks follow key = e L + (L - 1 - l), so an entry's rank is
+//   (emitted entries whose window ends before e0) + (its position among the range's entries),
+// the first term the sum of the lists' lower bounds at floor(e0 / p^l) (less the parents below
+// them in replace mode), the second an exclusive scan over a flag per (e - e0, L - 1 - l). The
+// workgroup then writes slot for every pyramid entry of its range (its rank, or -1) and idx for
+// the emitted ones. No workgroup depends on another.
 template <int NL>  // NL = L
 __global__ void __launch_bounds__(256) order_kernel(OrdArgs a) {
-  const int64_t gpos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (gpos >= a.Scand) return;
+  constexpr int NF = kOrdE * NL;  // flags of the range, one bit each
+  constexpr int NW = NF / 32;     // flag words
+  constexpr int NS = 3 * NL;      // lower bounds to find: lo, hi, parents below (replace)
+  constexpr int NSW = (NS + 3) / 4;
+  __shared__ uint32_t fl[NW];
+  __shared__ uint16_t wpre[NW];  // emitted entries of the range before flag word w
+  __shared__ int32_t bnd[NS];
+  __shared__ int32_t wsum[4];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t bh = blockIdx.y;
   const int32_t* C = a.ws + bh * a.Scand;
-  int l = 0;
-  while (l + 1 < a.L && gpos >= a.coff[l + 1]) ++l;
-  const int64_t i = C[gpos];
-  if (a.replace && l >= 1) {
-    // a parent's children are in the next finer candidate list; parents are not emitted
-    const int64_t c = lower_bound_val(C + a.coff[l - 1], a.cand[l - 1], i * a.p);
-    if (c < a.cand[l - 1] && C[a.coff[l - 1] + c] == i * a.p) return;
-  }
-  const int64_t K = order_key(i, l, a);
-  // The binary searches of the L lists run in lockstep: each step issues one independent probe
-  // per list, so a thread waits for about log2(max list) loads instead of L times as many.
-  // In its own list the entry's lower bound is its position (keys of a level increase with i).
-  int32_t lo[NL], hi[NL];
+  const int32_t e0 = (int32_t)blockIdx.x * kOrdE;
+  const int32_t e1 = a.N - e0 < kOrdE ? a.N : e0 + kOrdE;
+  for (int x = tid; x < NW; x += blockDim.x) fl[x] = 0u;
+  // Lower bounds, 64-ary per wave: search j = wv + 4 r. j < NL: list j at floor(e0 / p^j);
+  // j < 2 NL: list j - NL at floor(e1 / p^(j - NL)); else (replace, l = j - 2 NL >= 1): list
+  // l - 1 at p floor(e0 / p^l), whose children count gives the parents of level l below e0.
+  {
+    int32_t slo[NSW], shi[NSW], sl[NSW], sx[NSW];
 #pragma unroll
-  for (int l2 = 0; l2 < NL; ++l2) {
-    lo[l2] = l2 == l ? (int32_t)(gpos - a.coff[l]) : 0;
-    hi[l2] = l2 == l ? lo[l2] : (int32_t)a.cand[l2];
-  }
-  lockstep_search<NL>(lo, hi, a, [&](int l2, int32_t v) { return order_key(v, l2, a) < K; });
-  int64_t rank = 0;
+    for (int r = 0; r < NSW; ++r) {
+      const int j = wv + 4 * r;
+      const int l = j < NL ? j : j < 2 * NL ? j - NL : j - 2 * NL;
+      bool live = j < NS;
+      if (j >= 2 * NL) live = live && a.replace && l >= 1;
+      sx[r] = j < NL ? div_pw(e0, l, a) : j < 2 * NL ? div_pw(e1, l, a) : div_pw(e0, l, a) * a.p;
+      sl[r] = j >= 2 * NL ? (l >= 1 ? l - 1 : 0) : l;
+      slo[r] = 0;
+      shi[r] = live ? a.cand[sl[r]] : 0;
+    }
+    for (;;) {
+      bool open = false;
+      int32_t v[NSW];
 #pragma unroll
-  for (int l2 = 0; l2 < NL; ++l2) rank += lo[l2];
-  if (a.replace) {
-    // a selected parent is replaced by its children: the children below K are counted at the
-    // finer level, so the parents below K (those whose first child is below K) are taken off
-    int32_t lo2[NL], hi2[NL];
-    int32_t bound[NL + 1];  // first entry of list l2 at or after K (or the row count past the end)
+      for (int r = 0; r < NSW; ++r) {
+        v[r] = 0;
+        if (slo[r] < shi[r]) {  // uniform over the wave
+          const int32_t st = (shi[r] - slo[r] + 63) >> 6;
+          const int32_t pos = slo[r] + lane * st;
+          if (pos < shi[r]) v[r] = C[a.coff[sl[r]] + pos];
+          open = true;
+        }
+      }
+      if (!open) break;
 #pragma unroll
-    for (int l2 = 0; l2 <= NL; ++l2) bound[l2] = 0;
-#pragma unroll
-    for (int l2 = 0; l2 < NL; ++l2) {
-      lo2[l2] = hi2[l2] = 0;
-      if (l2 >= 1) {
-        const int32_t* c2 = C + a.coff[l2];
-        bound[l2] = lo[l2] < a.cand[l2] ? c2[lo[l2]] : (int32_t)a.nrows[l2];
-        hi2[l2 - 1] = (int32_t)a.cand[l2 - 1];
+      for (int r = 0; r < NSW; ++r) {
+        if (slo[r] < shi[r]) {
+          const int32_t n = shi[r] - slo[r], st = (n + 63) >> 6, T = (n + st - 1) / st;
+          const int32_t pos = slo[r] + lane * st;
+          const bool below = pos < shi[r] && v[r] < sx[r];
+          const int32_t c = (int32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(below));
+          const int32_t nlo = c > 0 ? slo[r] + (c - 1) * st + 1 : slo[r];
+          const int32_t nhi = c < T ? slo[r] + c * st : shi[r];
+          slo[r] = nlo, shi[r] = nhi;
+        }
       }
     }
-    // lists l2 - 1 are searched for bound[l2] * p (slot l2 - 1 of lo2 / hi2)
-    lockstep_search<NL>(lo2, hi2, a, [&](int l2, int32_t v) { return (int64_t)v < (int64_t)bound[l2 + 1] * a.p; });
 #pragma unroll
-    for (int l2 = 0; l2 + 1 < NL; ++l2) rank -= lo2[l2] / a.p;
+    for (int r = 0; r < NSW; ++r) {
+      const int j = wv + 4 * r;
+      if (lane == 0 && j < NS) bnd[j] = slo[r];
+    }
   }
-  if (rank < 0 || rank >= a.S) return;  // cannot happen for lists written by select_kernel
-  a.idx[bh * a.S + rank] = (int32_t)(a.off[l] + i);
-  a.slot[bh * a.Ptot + a.off[l] + i] = (int32_t)rank;
-}
-
-__global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += (int64_t)gridDim.x * blockDim.x)
-    p[t] = v;
+  __syncthreads();
+  // flag every emitted entry of the range (a parent is not emitted in replace mode); a thread
+  // loads MB list entries before marking any, so their loads are in flight together
+  int total = 0;
+#pragma unroll
+  for (int l = 0; l < NL; ++l) total += bnd[NL + l] - bnd[l];
+  constexpr int MB = 4;
+  for (int t0 = 0; t0 < total; t0 += MB * (int)blockDim.x) {
+    int32_t iv[MB], lv[MB];
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      const int t = t0 + m * (int)blockDim.x + tid;
+      lv[m] = -1;
+      iv[m] = 0;
+      if (t < total) {
+        int l = 0, u = t;
+        while (u >= bnd[NL + l] - bnd[l]) u -= bnd[NL + l] - bnd[l], ++l;
+        lv[m] = l;
+        iv[m] = C[a.coff[l] + bnd[l] + u];
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      const int l = lv[m];
+      if (l < 0) continue;
+      const int32_t i = iv[m];
+      if (a.replace && l >= 1) {
+        // a parent's children are in the next finer candidate list
+        const int64_t c = lower_bound_val(C + a.coff[l - 1], a.cand[l - 1], (int64_t)i * a.p);
+        if (c < a.cand[l - 1] && C[a.coff[l - 1] + c] == i * a.p) continue;
+      }
+      const int x = ((i + 1) * a.pw[l] - 1 - e0) * NL + (NL - 1 - l);
+      atomicOr(&fl[x >> 5], 1u << (x & 31));
+    }
+  }
+  __syncthreads();
+  // exclusive scan of the flags by words: thread tid owns words [tid CW, tid CW + CW)
+  constexpr int CW = NW / 256;
+  static_assert(NW % 256 == 0 && NF <= 65536, "words split evenly over 256 threads; ranks fit 16 bits");
+  int run = 0;
+#pragma unroll
+  for (int x = 0; x < CW; ++x) run += (int)__builtin_popcount(fl[tid * CW + x]);
+  int inc = run;  // inclusive scan over the wave
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int y = __shfl_up(inc, d, 64);
+    if (lane >= d) inc += y;
+  }
+  if (lane == 63) wsum[wv] = inc;
+  __syncthreads();
+  int base = inc - run;
+  for (int w = 0; w < wv; ++w) base += wsum[w];
+#pragma unroll
+  for (int x = 0; x < CW; ++x) {
+    wpre[tid * CW + x] = (uint16_t)base;
+    base += (int)__builtin_popcount(fl[tid * CW + x]);
+  }
+  // emitted entries whose window ends before e0
+  int32_t r0 = 0;
+#pragma unroll
+  for (int l = 0; l < NL; ++l) {
+    r0 += bnd[l];
+    if (a.replace && l >= 1) r0 -= bnd[2 * NL + l] / a.p;
+  }
+  __syncthreads();
+  // slot of every pyramid entry of the range; idx of the emitted ones
+  int32_t* idxh = a.idx + bh * a.S;
+  int32_t* sloth = a.slot + bh * a.Ptot;
+#pragma unroll
+  for (int l = 0; l < NL; ++l) {
+    const int32_t i0 = div_pw(e0, l, a), i1 = div_pw(e1, l, a);
+    for (int32_t i = i0 + tid; i < i1; i += blockDim.x) {
+      const int x = ((i + 1) * a.pw[l] - 1 - e0) * NL + (NL - 1 - l);
+      const uint32_t word = fl[x >> 5], sh = (uint32_t)(x & 31);
+      int32_t out = -1;
+      if ((word >> sh) & 1u) {
+        const int32_t rr = r0 + wpre[x >> 5] + (int32_t)__builtin_popcount(word & ((1u << sh) - 1u));
+        if (rr < a.S) {  // cannot fail for lists written by select_kernel
+          out = rr;
+          idxh[rr] = a.off[l] + i;
+        }
+      }
+      sloth[a.off[l] + i] = out;
+    }
+  }
 }
 
 }  // namespace lh
@@ -397,14 +474,6 @@ using namespace lh;
 hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_kq, int32_t* idx,
                             int32_t* slot, int32_t* ws, hipStream_t st) {
   const int64_t BH = s.B * s.Hs;  // one selection per (b, selection head)
-  // slot = -1 everywhere (a fill kernel, so the sequence can be captured in a graph)
-  {
-    const int64_t n = BH * s.Ptot;
-    int64_t blocks = (n + 255) / 256;
-    if (blocks > 65536) blocks = 65536;
-    if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(fill_i32_kernel, dim3((unsigned)blocks), dim3(256), 0, st, slot, n, -1);
-  }
   SelArgs a;
   a.s_qk = s_qk;
   a.s_kq = s_kq;
@@ -436,15 +505,23 @@ hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_
   o.ws = ws;
   o.idx = idx;
   o.slot = slot;
-  o.Ptot = s.Ptot;
   o.Scand = s.Scand;
-  o.S = s.S;
+  o.Ptot = (int32_t)s.Ptot;
+  o.S = (int32_t)s.S;
+  o.N = (int32_t)s.N;
   o.L = s.L;
   o.p = s.p;
   o.replace = (s.flags & LH_FLAG_REPLACE_PARENTS) ? 1 : 0;
-  for (int l = 0; l < 17; ++l) o.off[l] = s.off[l], o.coff[l] = s.coff[l];
-  for (int l = 0; l < 16; ++l) o.pw[l] = s.pw[l], o.cand[l] = s.cand[l], o.nrows[l] = l < s.L ? s.N / s.pw[l] : 0;
-  dim3 grid((unsigned)((s.Scand + 255) / 256), (unsigned)BH);
+  int pl = 0;
+  while ((1 << pl) < s.p) ++pl;
+  const bool pow2 = (1 << pl) == s.p;
+  for (int l = 0; l < 17; ++l) o.off[l] = (int32_t)s.off[l], o.coff[l] = (int32_t)s.coff[l];
+  for (int l = 0; l < 16; ++l) {
+    o.pw[l] = l < s.L ? (int32_t)s.pw[l] : 1;
+    o.cand[l] = (int32_t)s.cand[l];
+    o.lsh[l] = pow2 ? l * pl : -1;
+  }
+  dim3 grid((unsigned)((s.N + kOrdE - 1) / kOrdE), (unsigned)BH);
   switch (s.L) {
     case 1: hipLaunchKernelGGL(order_kernel<1>, grid, dim3(256), 0, st, o); break;
     case 2: hipLaunchKernelGGL(order_kernel<2>, grid, dim3(256), 0, st, o); break;

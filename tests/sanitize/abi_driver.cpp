@@ -203,7 +203,7 @@ int main() {
       mk(1, 1024, 2, 2, 64, 4, 3, -1, LH_F32, 0),   mk(1, 1024, 3, 2, 64, 4, 3, 128, LH_F32, 0),
       mk(1, 1024, 2, 2, 96, 4, 3, 128, LH_F32, 0),  mk(1, 1024, 2, 2, 64, 4, 3, 128, 7, 0),
       mk(1, 1024, 2, 2, 64, 4, 3, 128, LH_F32, 8),  mk(0, 1024, 2, 2, 64, 4, 3, 128, LH_F32, 0),
-      mk(1, 1 << 20, 2, 2, 64, 4, 2, 1000, LH_F32, 0), mk(1, (int64_t)1 << 31, 1, 1, 64, 2, 2, 1, LH_F32, 0),
+      mk(1, (int64_t)1 << 28, 1, 1, 64, 2, 2, 1, LH_F32, 0), mk(1, (int64_t)1 << 31, 1, 1, 64, 2, 2, 1, LH_F32, 0),
       mk(1, 1024, 2, 2, 64, 4, 3, 128, LH_F32, 0) /* scale set below */,
   };
   const int n_invalid = (int)(sizeof(invalid) / sizeof(invalid[0]));

@@ -395,9 +395,82 @@ def test_selection_workspace_math(name, c, flags):
     # of maxsel keys per selection after the lists
     if s.maxsel > 32768:
         inside("select key rows", BH * s.Scand, BH * s.Scand + BH * s.maxsel, ws_bytes // 4)
-    # order_kernel: grid ((Scand + 255) / 256, BH); entries t < Scand of list bs
-    gx = -(-s.Scand // 256)
-    t = np.arange(gx * 256)
-    once("order entries", t[t < s.Scand], s.Scand)
+    # order_kernel: grid ((N + 8191) / 8192, BH); workgroup x owns the window ends [e0, e1) and
+    # the level-l entries [e0 // p^l, e1 // p^l): every pyramid entry's slot is written by
+    # exactly one workgroup, and its flag index (end - e0) L + (L - 1 - l) stays in [0, 8192 L)
+    E = 8192
+    gx = -(-s.N // E)
+    e0 = np.arange(gx, dtype=np.int64) * E
+    e1 = np.minimum(e0 + E, s.N)
+    assert e0.max() < 2 ** 31 and (e1 > e0).all()
+    for l in range(s.L):
+        lo, hi = e0 // s.pw[l], e1 // s.pw[l]
+        ids = np.concatenate([np.arange(a, b) for a, b in zip(lo, hi)])
+        once(f"order slot entries l{l}", ids, s.nrow[l])
+        blk = np.repeat(np.arange(gx), hi - lo)
+        x = ((ids + 1) * s.pw[l] - 1 - e0[blk]) * s.L + (s.L - 1 - l)
+        inside(f"order flag index l{l}", x, x + 1, E * s.L)
     # every emitted entry gets a distinct rank in [0, S)
     assert s.S <= s.Scand
+
+
+def _order_by_ranges(N, p, L, lists, replace, E=8192):
+    """order_kernel's ranking, restated on the CPU: per range of window ends, the emitted
+    entries before it (lower bounds in the sorted lists, less the parents below them in replace
+    mode) plus an exclusive scan over the range's (end, level) flags."""
+    pw = [p ** l for l in range(L)]
+    out = {}
+    for e0 in range(0, N, E):
+        e1 = min(e0 + E, N)
+        r0 = 0
+        for l in range(L):
+            r0 += int(np.searchsorted(lists[l], e0 // pw[l]))
+            if replace and l >= 1:
+                r0 -= int(np.searchsorted(lists[l - 1], (e0 // pw[l]) * p)) // p
+        flag = np.zeros(E * L, np.int64)
+        ent = {}
+        for l in range(L):
+            a, b = np.searchsorted(lists[l], [e0 // pw[l], e1 // pw[l]])
+            for i in lists[l][a:b]:
+                i = int(i)
+                if replace and l >= 1:
+                    c = int(np.searchsorted(lists[l - 1], i * p))
+                    if c < len(lists[l - 1]) and lists[l - 1][c] == i * p:
+                        continue
+                x = ((i + 1) * pw[l] - 1 - e0) * L + (L - 1 - l)
+                flag[x] = 1
+                ent[x] = (l, i)
+        rank = np.cumsum(flag) - flag
+        for x, li in ent.items():
+            out[li] = r0 + int(rank[x])
+    return out
+
+
+@pytest.mark.parametrize("N,p,L,k,replace,seed", [(4096, 4, 4, 100, False, 1), (4096, 4, 4, 100, True, 2),
+                                                  (3000, 5, 3, 40, False, 3), (3000, 5, 3, 40, True, 4),
+                                                  (2048, 2, 8, 12, True, 5), (1000, 2, 1, 0, False, 6),
+                                                  (8192, 4, 5, 0, False, 7), (5120, 4, 3, 2000, True, 8)])
+def test_order_ranges_match_sorted_keys(N, p, L, k, replace, seed):
+    """The range-wise ranking equals sorting the emitted entries by key = e L + (L - 1 - l),
+    e = (i + 1) p^l - 1, for selections of the structure select_kernel writes (the coarsest
+    level whole; each level's candidates the children of the k best of the level above)."""
+    rng = np.random.default_rng(seed)
+    lists = [None] * L
+    lists[L - 1] = np.arange(N // p ** (L - 1))
+    for l in range(L - 1, 0, -1):
+        npar = min(k, len(lists[l]))
+        par = np.sort(rng.choice(lists[l], npar, replace=False))
+        lists[l - 1] = (par[:, None] * p + np.arange(p)[None, :]).ravel()
+    # the kernel's ranges of 8192 window ends, and short ones that split coarse windows
+    got = _order_by_ranges(N, p, L, lists, replace)
+    assert got == _order_by_ranges(N, p, L, lists, replace, E=64)
+    emitted = []
+    for l in range(L):
+        child = set(lists[l - 1].tolist()) if (replace and l >= 1) else set()
+        for i in lists[l].tolist():
+            if i * p in child:
+                continue
+            emitted.append((((i + 1) * p ** l - 1) * L + (L - 1 - l), l, i))
+    emitted.sort()
+    want = {(l, i): r for r, (_, l, i) in enumerate(emitted)}
+    assert got == want
