@@ -34,6 +34,9 @@ constexpr int kSelWaves = kSelThreads / 64;
 // them in a global workspace region of their own (one row of maxsel keys per selection), which
 // the radix passes stream through L2.
 constexpr int64_t kSelLdsKeys = 32768;
+// Candidate lists of levels >= 1 of at most this many entries stay in LDS beside the keys
+// (LL mode: 2 x 64 KB).
+constexpr int64_t kSelLdsList = 16384;
 
 struct SelArgs {
   const float* s_qk;
@@ -85,9 +88,14 @@ __device__ __forceinline__ void select_bin(const int* hist, uint32_t* sel_state,
 
 // GK: the level's keys live in the global rows a.gkeys (levels above kSelLdsKeys candidates)
 // instead of LDS; the algorithm is the same.
-template <bool GK>
+// LL (lists in LDS, when every list of levels >= 1 has at most kSelLdsList entries): the
+// candidate list of the current level is also kept in LDS, after the keys, so the id reads of
+// the key load and of the compaction make no global round trip. The lists are still written to
+// the workspace, where the order kernel reads them.
+template <bool GK, bool LL>
 __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
-  extern __shared__ uint32_t keys_lds[];  // candidate keys of the current level
+  static_assert(!(GK && LL), "lists in LDS go with keys in LDS");
+  extern __shared__ uint32_t keys_lds[];  // candidate keys of the current level (LL: then its list)
   __shared__ __align__(16) int hist[256];
   __shared__ uint32_t sel_state[2];  // prefix, remaining
   __shared__ int wave_gt[kSelWaves], wave_eq[kSelWaves];  // counts of each wave's candidates
@@ -103,23 +111,39 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
   const float* sk = a.s_kq + (b * a.Hkv + g) * a.Ptot;
   int32_t* C = a.ws + (int64_t)bs * a.Scand;
   uint32_t* keys = GK ? a.gkeys + (int64_t)bs * a.maxsel : keys_lds;
+  int32_t* list = reinterpret_cast<int32_t*>(keys_lds) + kSelLdsList;  // LL only
   const int L = a.L, p = a.p;
 
   // top level: every entry is a candidate
-  for (int64_t u = tid; u < a.cand[L - 1]; u += kSelThreads) C[a.coff[L - 1] + u] = (int32_t)u;
+  for (int64_t u = tid; u < a.cand[L - 1]; u += kSelThreads) {
+    C[a.coff[L - 1] + u] = (int32_t)u;
+    if (LL && L > 1) list[u] = (int32_t)u;
+  }
   __threadfence_block();
   __syncthreads();
 
   for (int l = L - 1; l >= 1; --l) {
     const int64_t n = a.cand[l];
     const int64_t kk = a.npar[l];
-    const int32_t* Cl = C + a.coff[l];
+    const int32_t* Cl = LL ? list : C + a.coff[l];
     int32_t* Cn = C + a.coff[l - 1];
+    const bool ln = LL && l - 1 >= 1;  // the next level's list is kept in LDS too
     const float* sql = sq + a.off[l];
     const float* skl = sk + a.off[l];
     if (kk == n) {
       // every candidate is a parent
-      for (int64_t j = tid; j < n * p; j += kSelThreads) Cn[j] = Cl[j / p] * p + (int32_t)(j % p);
+      if (LL) {
+        // the list is expanded in place: copy it to the (unused) key buffer first
+        for (int64_t u = tid; u < n; u += kSelThreads) keys[u] = (uint32_t)list[u];
+        __syncthreads();
+        for (int64_t j = tid; j < n * p; j += kSelThreads) {
+          const int32_t v = (int32_t)keys[j / p] * p + (int32_t)(j % p);
+          Cn[j] = v;
+          if (ln) list[j] = v;
+        }
+      } else {
+        for (int64_t j = tid; j < n * p; j += kSelThreads) Cn[j] = Cl[j / p] * p + (int32_t)(j % p);
+      }
       __threadfence_block();
       __syncthreads();
       continue;
@@ -262,7 +286,12 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
         if (gt || (eq && er < need)) {
           const int64_t pos = first + gr + (er < need ? er : need);
           const int32_t i = (int32_t)(e & 0x3fffffffu);
-          for (int r = 0; r < p; ++r) Cn[pos * p + r] = i * p + r;
+          for (int r = 0; r < p; ++r) {
+            Cn[pos * p + r] = i * p + r;
+            // one chunk: every id of the level was read before this pass, so the list can be
+            // overwritten in place (several chunks reload it after the level)
+            if (ln && !a.stratified) list[pos * p + r] = i * p + r;
+          }
         }
         gt_rank += __popcll(bg);
         eq_rank += __popcll(be);
@@ -271,6 +300,10 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
     }
     __threadfence_block();
     __syncthreads();
+    if (ln && a.stratified) {  // the next level's list, from the workspace just written
+      for (int64_t u = tid; u < a.cand[l - 1]; u += kSelThreads) list[u] = Cn[u];
+      __syncthreads();
+    }
   }
 }
 
@@ -492,11 +525,16 @@ hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_
   a.stratified = (s.flags & LH_FLAG_STRATIFIED) ? 1 : 0;
   a.maxsel = s.maxsel;
   a.gkeys = s.maxsel > kSelLdsKeys ? reinterpret_cast<uint32_t*>(ws + BH * s.Scand) : nullptr;
+  int64_t lmax = 0;  // the longest list select_kernel reads (levels >= 1)
+  for (int l = 1; l < s.L; ++l) lmax = s.cand[l] > lmax ? s.cand[l] : lmax;
   if (a.gkeys) {
-    hipLaunchKernelGGL(select_kernel<true>, dim3((unsigned)BH), dim3(kSelThreads), 0, st, a);
+    hipLaunchKernelGGL((select_kernel<true, false>), dim3((unsigned)BH), dim3(kSelThreads), 0, st, a);
+  } else if (lmax <= kSelLdsList && s.maxsel <= kSelLdsList) {
+    const size_t shm = 2 * (size_t)kSelLdsList * sizeof(uint32_t);
+    hipLaunchKernelGGL((select_kernel<false, true>), dim3((unsigned)BH), dim3(kSelThreads), shm, st, a);
   } else {
     const size_t shm = (size_t)(s.maxsel > 0 ? s.maxsel : 1) * sizeof(uint32_t);
-    hipLaunchKernelGGL(select_kernel<false>, dim3((unsigned)BH), dim3(kSelThreads), shm, st, a);
+    hipLaunchKernelGGL((select_kernel<false, false>), dim3((unsigned)BH), dim3(kSelThreads), shm, st, a);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
