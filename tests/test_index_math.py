@@ -161,7 +161,7 @@ class RunLaunch:
         self.run = s.p if s.L > 1 else 1
         self.nruns = s.N // self.run + (1 if scatter else 0)
         self.HC = H << s.cs
-        self.bs = min(self.HC, 256)
+        self.bs = min(self.HC, 512)
         self.nx = -(-self.nruns // 8) * 8
         self.gy = -(-self.HC // self.bs)
         self.rpb = 1
