@@ -245,26 +245,29 @@ __device__ __forceinline__ BlockPos block_pos() {
 }
 
 struct RowSrc {
-  const bf16_t* l0;  // row 0 of the head in the input
-  const bf16_t* py;  // row 0 of the head in the pyramid
-  int64_t st;        // elements between consecutive rows: H * D
-  int32_t N, last;   // last = N + R - 1
+  const char* l0;  // row 0 of the head in the input
+  const char* py;  // row 0 of the head in the pyramid, less N rows: pyramid id i is at py + i rb
+  uint32_t rb;     // bytes between consecutive rows: H * D * 2
+  int32_t N, last;  // last = N + R - 1
 };
 
 __device__ __forceinline__ RowSrc row_src(const bf16_t* x, const bf16_t* pyr, int64_t b, int h, int H,
                                           const SdpaIdx& ix, int D) {
   RowSrc r;
-  r.st = (int64_t)H * D;
-  r.l0 = x + (b * ix.N * H + h) * D;
-  r.py = pyr + (b * ix.R * H + h) * D;
+  r.rb = (uint32_t)(H * D * 2);
+  r.l0 = reinterpret_cast<const char*>(x + (b * ix.N * H + h) * D);
+  r.py = reinterpret_cast<const char*>(pyr + (b * ix.R * H + h) * D) - (int64_t)ix.N * r.rb;
   r.N = (int32_t)ix.N;
   r.last = (int32_t)(ix.N + ix.R - 1);
   return r;
 }
 
+// One clamp (a median of three), one compare with two selects for the base, one 32 x 32 -> 64-bit
+// multiply-add.
 __device__ __forceinline__ const bf16_t* rs_row(const RowSrc& s, int32_t id) {
   id = id < 0 ? 0 : id > s.last ? s.last : id;
-  return id < s.N ? s.l0 + (int64_t)id * s.st : s.py + (int64_t)(id - s.N) * s.st;
+  const char* base = id < s.N ? s.l0 : s.py;
+  return reinterpret_cast<const bf16_t*>(base + (uint64_t)(uint32_t)id * s.rb);
 }
 
 // Pyramid ids of the rows this lane copies in load_tile (rows past S take row S - 1's id).
