@@ -114,7 +114,12 @@ def test_select_fig2_toy():
                                            # levels of 40,000 and 131,072 candidates: keys in the
                                            # workspace instead of LDS
                                            (262144, 4, 3, 10000, 0), (262144, 4, 3, 10000, 2),
-                                           (262144, 2, 2, 50000, 1)])
+                                           (262144, 2, 2, 50000, 1),
+                                           # several ranges of 8,192 window ends in the order
+                                           # kernel that split coarse windows (p = 3, 5), with
+                                           # and without replace mode
+                                           (19683, 3, 4, 500, 1), (20000, 5, 3, 300, 0),
+                                           (20000, 5, 3, 300, 1), (59049, 3, 3, 3000, 3)])
 def test_select_random_scores(N, p, L, k, flags, ties, rng):
     Hq, Hkv = 4, 2
     print(f"[stage select] N={N} p={p} L={L} k={k} flags={flags} ties={ties}", flush=True)
