@@ -75,7 +75,8 @@ typedef enum {
   LH_E_DTYPE = -4,      /* dtype not supported by this entry point                    */
   LH_E_ALIGN = -5,      /* a pointer is not 16-byte aligned                           */
   LH_E_WORKSPACE = -6,  /* workspace missing or smaller than lh_workspace_bytes()     */
-  LH_E_HIP = -7         /* the HIP runtime reported an error while enqueueing         */
+  LH_E_HIP = -7,        /* the HIP runtime reported an error while enqueueing         */
+  LH_E_NONFINITE = -8   /* a floating-point argument (the softmax scale) is NaN or inf */
 } lh_status;
 
 typedef enum { LH_F32 = 0, LH_BF16 = 1 } lh_dtype;

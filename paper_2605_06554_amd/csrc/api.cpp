@@ -37,8 +37,9 @@ lh_status make_shape(const lh_problem* pr, LhShape* s) {
   if (pr->dtype != LH_F32 && pr->dtype != LH_BF16) return fail(LH_E_DTYPE, "dtype must be LH_F32 or LH_BF16 (%d)", pr->dtype);
   if (pr->flags & ~(uint32_t)(LH_FLAG_REPLACE_PARENTS | LH_FLAG_STRATIFIED | LH_FLAG_GQA_SHARED))
     return fail(LH_E_PARAM, "unknown flag bits 0x%x", pr->flags);
-  if (!(pr->scale >= 0.0f) || isinf(pr->scale))
-    return fail(LH_E_PARAM, "scale must be finite and >= 0 (0 selects 1/sqrt(D))");
+  if (isnan(pr->scale) || isinf(pr->scale))
+    return fail(LH_E_NONFINITE, "scale must be finite (0 selects 1/sqrt(D))");
+  if (pr->scale < 0.0f) return fail(LH_E_PARAM, "scale must be >= 0 (0 selects 1/sqrt(D))");
   memset(s, 0, sizeof(*s));
   s->B = pr->B;
   s->N = pr->N;
@@ -247,6 +248,7 @@ const char* lh_status_str(lh_status st) {
     case LH_E_ALIGN: return "LH_E_ALIGN";
     case LH_E_WORKSPACE: return "LH_E_WORKSPACE";
     case LH_E_HIP: return "LH_E_HIP";
+    case LH_E_NONFINITE: return "LH_E_NONFINITE";
     default: return "LH_E_UNKNOWN";
   }
 }

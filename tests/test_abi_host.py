@@ -51,7 +51,8 @@ def _pr(**kw):
     (dict(N=2 ** 20, L=2, k=1000), 0),   # a level of 262144 candidates ranks with its keys in the workspace
     (dict(N=2 ** 28, p=2, L=2, k=1), -3),  # 2^27 candidates at one level: beyond the 2^26 supported
     (dict(scale=-0.125), -3),           # a negative softmax scale is refused
-    (dict(scale=float("nan")), -3),
+    (dict(scale=float("nan")), -8),     # a non-finite scale: LH_E_NONFINITE
+    (dict(scale=float("inf")), -8),
 ])
 def test_check_codes(kw, code):
     pr = _pr(**kw)
