@@ -52,6 +52,7 @@ struct SelArgs {
   int64_t npar[16];
   int64_t coff[17];
   int32_t stratified;  // LH_FLAG_STRATIFIED: per-chunk shares instead of one top-k per level
+  int32_t coff_aligned4;  // every coff[l] is a multiple of 4
 };
 
 // One wave picks the digit of the quota-th largest key from the 256-bin histogram: the highest
@@ -95,7 +96,7 @@ __device__ __forceinline__ void select_bin(const int* hist, uint32_t* sel_state,
 template <bool GK, bool LL>
 __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
   static_assert(!(GK && LL), "lists in LDS go with keys in LDS");
-  extern __shared__ uint32_t keys_lds[];  // candidate keys of the current level (LL: then its list)
+  extern __shared__ __align__(16) uint32_t keys_lds[];  // candidate keys of the current level (LL: then its list)
   __shared__ __align__(16) int hist[256];
   __shared__ uint32_t sel_state[2];  // prefix, remaining
   __shared__ int wave_gt[kSelWaves], wave_eq[kSelWaves];  // counts of each wave's candidates
@@ -112,14 +113,18 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
   int32_t* C = a.ws + (int64_t)bs * a.Scand;
   uint32_t* keys = GK ? a.gkeys + (int64_t)bs * a.maxsel : keys_lds;
   int32_t* list = reinterpret_cast<int32_t*>(keys_lds) + kSelLdsList;  // LL only
+  // children of a parent as one 16-byte store: every list of this selection's workspace row
+  // starts 16-byte aligned
+  const bool vec4 = ((reinterpret_cast<uintptr_t>(C) & 15) == 0) && a.coff_aligned4;
   const int L = a.L, p = a.p;
 
-  // top level: every entry is a candidate
+  // Top level: every entry is a candidate. With LL the lists written to the workspace are read
+  // only after the kernel (by the order kernel), so no level waits for its global writes.
   for (int64_t u = tid; u < a.cand[L - 1]; u += kSelThreads) {
     C[a.coff[L - 1] + u] = (int32_t)u;
     if (LL && L > 1) list[u] = (int32_t)u;
   }
-  __threadfence_block();
+  if (!LL) __threadfence_block();
   __syncthreads();
 
   for (int l = L - 1; l >= 1; --l) {
@@ -136,15 +141,24 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
         // the list is expanded in place: copy it to the (unused) key buffer first
         for (int64_t u = tid; u < n; u += kSelThreads) keys[u] = (uint32_t)list[u];
         __syncthreads();
-        for (int64_t j = tid; j < n * p; j += kSelThreads) {
-          const int32_t v = (int32_t)keys[j / p] * p + (int32_t)(j % p);
-          Cn[j] = v;
-          if (ln) list[j] = v;
+        if (p == 4 && vec4) {  // one parent per thread: its 4 children as one 16-byte store
+          for (int64_t u = tid; u < n; u += kSelThreads) {
+            const int32_t c0 = (int32_t)keys[u] * 4;
+            const u32x4 v = {(uint32_t)c0, (uint32_t)c0 + 1u, (uint32_t)c0 + 2u, (uint32_t)c0 + 3u};
+            *reinterpret_cast<u32x4*>(Cn + 4 * u) = v;
+            if (ln) *reinterpret_cast<u32x4*>(list + 4 * u) = v;
+          }
+        } else {
+          for (int64_t j = tid; j < n * p; j += kSelThreads) {
+            const int32_t v = (int32_t)keys[j / p] * p + (int32_t)(j % p);
+            Cn[j] = v;
+            if (ln) list[j] = v;
+          }
         }
       } else {
         for (int64_t j = tid; j < n * p; j += kSelThreads) Cn[j] = Cl[j / p] * p + (int32_t)(j % p);
       }
-      __threadfence_block();
+      if (!LL) __threadfence_block();
       __syncthreads();
       continue;
     }
@@ -286,11 +300,17 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
         if (gt || (eq && er < need)) {
           const int64_t pos = first + gr + (er < need ? er : need);
           const int32_t i = (int32_t)(e & 0x3fffffffu);
-          for (int r = 0; r < p; ++r) {
-            Cn[pos * p + r] = i * p + r;
-            // one chunk: every id of the level was read before this pass, so the list can be
-            // overwritten in place (several chunks reload it after the level)
-            if (ln && !a.stratified) list[pos * p + r] = i * p + r;
+          // one chunk: every id of the level was read before this pass, so the list can be
+          // overwritten in place (several chunks reload it after the level)
+          if (p == 4 && vec4) {
+            const u32x4 v = {(uint32_t)(i * 4), (uint32_t)(i * 4 + 1), (uint32_t)(i * 4 + 2), (uint32_t)(i * 4 + 3)};
+            *reinterpret_cast<u32x4*>(Cn + pos * 4) = v;
+            if (ln && !a.stratified) *reinterpret_cast<u32x4*>(list + pos * 4) = v;
+          } else {
+            for (int r = 0; r < p; ++r) {
+              Cn[pos * p + r] = i * p + r;
+              if (ln && !a.stratified) list[pos * p + r] = i * p + r;
+            }
           }
         }
         gt_rank += __popcll(bg);
@@ -298,7 +318,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
       }
       __syncthreads();  // sel_state and hist are reused by the next chunk
     }
-    __threadfence_block();
+    if (!LL || (ln && a.stratified)) __threadfence_block();
     __syncthreads();
     if (ln && a.stratified) {  // the next level's list, from the workspace just written
       for (int64_t u = tid; u < a.cand[l - 1]; u += kSelThreads) list[u] = Cn[u];
@@ -523,6 +543,8 @@ hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_
   for (int l = 0; l < 17; ++l) a.off[l] = s.off[l], a.coff[l] = s.coff[l];
   for (int l = 0; l < 16; ++l) a.cand[l] = s.cand[l], a.npar[l] = s.npar[l];
   a.stratified = (s.flags & LH_FLAG_STRATIFIED) ? 1 : 0;
+  a.coff_aligned4 = 1;
+  for (int l = 0; l <= s.L; ++l) a.coff_aligned4 &= (s.coff[l] % 4 == 0) ? 1 : 0;
   a.maxsel = s.maxsel;
   a.gkeys = s.maxsel > kSelLdsKeys ? reinterpret_cast<uint32_t*>(ws + BH * s.Scand) : nullptr;
   int64_t lmax = 0;  // the longest list select_kernel reads (levels >= 1)
