@@ -5,7 +5,7 @@
 // it ranks the level's candidates (a sorted list of level-local indices; their keys in LDS, or in
 // a global workspace row when a level has more than 32,768 candidates) by the 32-bit key
 // bits(max(s_QK, s_KQ)) -- non-negative floats, so the bit pattern orders them -- and finds the
-// exact threshold of the k best by an MSB-first radix select (8-bit digits below the bits all
+// exact threshold of the k best by an MSB-first radix select (11-bit digits below the bits all
 // keys share, LDS histograms with integer atomics; one wave reads each digit off the histogram
 // with a suffix scan). A stable compaction in candidate order then takes every key above the threshold and
 // the first (lower-index) ties, and writes the p children of each parent -- which are the next
@@ -55,31 +55,43 @@ struct SelArgs {
   int32_t coff_aligned4;  // every coff[l] is a multiple of 4
 };
 
-// One wave picks the digit of the quota-th largest key from the 256-bin histogram: the highest
-// bin whose count, added to the counts of every higher bin, reaches the remaining quota. The
-// remaining quota drops by the count of the higher bins. Lane l holds bins 4l .. 4l + 3; a
-// suffix sum over the lanes finds the one lane where the running count crosses the quota.
+// Radix digits of kDigitBits bits: kBins histogram bins.
+constexpr int kDigitBits = 11;
+constexpr int kBins = 1 << kDigitBits;
+constexpr int kBinsPerLane = kBins / 64;
+
+// One wave picks the digit of the quota-th largest key from the histogram: the highest bin
+// whose count, added to the counts of every higher bin, reaches the remaining quota. The
+// remaining quota drops by the count of the higher bins. Lane l holds bins kBinsPerLane l ..
+// kBinsPerLane (l + 1) - 1; a suffix sum over the lanes finds the one lane where the running
+// count crosses the quota, and that lane walks its bins from the top.
 __device__ __forceinline__ void select_bin(const int* hist, uint32_t* sel_state, uint32_t prefix, int shift,
                                            int lane) {
   const uint32_t rem = sel_state[1];
-  const int4 hb = *reinterpret_cast<const int4*>(hist + 4 * lane);
-  const uint32_t lsum = (uint32_t)(hb.x + hb.y + hb.z + hb.w);
-  uint32_t suf = lsum;  // counts of bins 4 lane .. 255
+  uint32_t c[kBinsPerLane];
+#pragma unroll
+  for (int q = 0; q < kBinsPerLane / 4; ++q) {
+    const int4 hb = *reinterpret_cast<const int4*>(hist + kBinsPerLane * lane + 4 * q);
+    c[4 * q] = (uint32_t)hb.x, c[4 * q + 1] = (uint32_t)hb.y, c[4 * q + 2] = (uint32_t)hb.z, c[4 * q + 3] = (uint32_t)hb.w;
+  }
+  uint32_t lsum = 0;
+#pragma unroll
+  for (int j = 0; j < kBinsPerLane; ++j) lsum += c[j];
+  uint32_t suf = lsum;  // counts of this lane's bins and every higher one
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
     const uint32_t t = __shfl_down(suf, d, 64);
     if (lane + d < 64) suf += t;
   }
-  const uint32_t above = suf - lsum;  // counts of bins 4 lane + 4 .. 255
-  const uint32_t c[4] = {(uint32_t)hb.x, (uint32_t)hb.y, (uint32_t)hb.z, (uint32_t)hb.w};
+  const uint32_t above = suf - lsum;  // counts of the bins above this lane's
   if (above < rem && above + lsum >= rem) {
     uint32_t acc = above;
-    int j = 3;
+    int j = kBinsPerLane - 1;
     for (; j > 0; --j) {
       if (acc + c[j] >= rem) break;
       acc += c[j];
     }
-    sel_state[0] = prefix | ((uint32_t)(4 * lane + j) << shift);
+    sel_state[0] = prefix | ((uint32_t)(kBinsPerLane * lane + j) << shift);
     sel_state[1] = rem - acc;
   } else if (lane == 0 && suf < rem) {  // fewer keys than the quota (not reached): bin 0
     sel_state[0] = prefix;
@@ -97,7 +109,7 @@ template <bool GK, bool LL>
 __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
   static_assert(!(GK && LL), "lists in LDS go with keys in LDS");
   extern __shared__ __align__(16) uint32_t keys_lds[];  // candidate keys of the current level (LL: then its list)
-  __shared__ __align__(16) int hist[256];
+  __shared__ __align__(16) int hist[kBins];
   __shared__ uint32_t sel_state[2];  // prefix, remaining
   __shared__ int wave_gt[kSelWaves], wave_eq[kSelWaves];  // counts of each wave's candidates
   __shared__ uint32_t key_and[kSelWaves], key_or[kSelWaves];  // per-wave AND / OR of the keys
@@ -232,10 +244,10 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelArgs a) {
         sel_state[1] = (uint32_t)quota;
       }
       __syncthreads();
-      // MSB-first radix select of the quota-th largest key of the chunk, 8 bits a pass
-      for (int hi = nb; hi > 0; hi -= 8) {
-        const int shift = hi > 8 ? hi - 8 : 0;
-        for (int t = tid; t < 256; t += kSelThreads) hist[t] = 0;
+      // MSB-first radix select of the quota-th largest key of the chunk, kDigitBits a pass
+      for (int hi = nb; hi > 0; hi -= kDigitBits) {
+        const int shift = hi > kDigitBits ? hi - kDigitBits : 0;
+        for (int t = tid; t < kBins; t += kSelThreads) hist[t] = 0;
         __syncthreads();
         const uint32_t prefix = sel_state[0];
         const uint32_t himask = hi == 32 ? 0u : (0xffffffffu << hi);
