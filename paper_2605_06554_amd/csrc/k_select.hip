@@ -368,9 +368,10 @@ __device__ __forceinline__ int64_t lower_bound_val(const int32_t* c, int64_t n, 
   return lo;
 }
 
-// Window ends per workgroup of order_kernel (a multiple of 8192 / L for every L, so that the
-// range's flag words split evenly over 256 threads).
+// Window ends and threads per workgroup of order_kernel.
 constexpr int kOrdE = 8192;
+constexpr int kOrdThreads = 512;
+constexpr int kOrdWaves = kOrdThreads / 64;
 
 // order_kernel: workgroup x of a selection owns the window ends e in [e0, e1), e0 = x kOrdE:
 // the level-l entries i in [floor(e0 / p^l), floor(e1 / p^l)), a contiguous part of each level's
@@ -381,29 +382,29 @@ constexpr int kOrdE = 8192;
 // workgroup then writes slot for every pyramid entry of its range (its rank, or -1) and idx for
 // the emitted ones. No workgroup depends on another.
 template <int NL>  // NL = L
-__global__ void __launch_bounds__(256) order_kernel(OrdArgs a) {
+__global__ void __launch_bounds__(kOrdThreads) order_kernel(OrdArgs a) {
   constexpr int NF = kOrdE * NL;  // flags of the range, one bit each
   constexpr int NW = NF / 32;     // flag words
   constexpr int NS = 3 * NL;      // lower bounds to find: lo, hi, parents below (replace)
-  constexpr int NSW = (NS + 3) / 4;
+  constexpr int NSW = (NS + kOrdWaves - 1) / kOrdWaves;
   __shared__ uint32_t fl[NW];
   __shared__ uint16_t wpre[NW];  // emitted entries of the range before flag word w
   __shared__ int32_t bnd[NS];
-  __shared__ int32_t wsum[4];
+  __shared__ int32_t wsum[kOrdWaves];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t bh = blockIdx.y;
   const int32_t* C = a.ws + bh * a.Scand;
   const int32_t e0 = (int32_t)blockIdx.x * kOrdE;
   const int32_t e1 = a.N - e0 < kOrdE ? a.N : e0 + kOrdE;
   for (int x = tid; x < NW; x += blockDim.x) fl[x] = 0u;
-  // Lower bounds, 64-ary per wave: search j = wv + 4 r. j < NL: list j at floor(e0 / p^j);
+  // Lower bounds, 64-ary per wave: search j = wv + kOrdWaves r. j < NL: list j at floor(e0 / p^j);
   // j < 2 NL: list j - NL at floor(e1 / p^(j - NL)); else (replace, l = j - 2 NL >= 1): list
   // l - 1 at p floor(e0 / p^l), whose children count gives the parents of level l below e0.
   {
     int32_t slo[NSW], shi[NSW], sl[NSW], sx[NSW];
 #pragma unroll
     for (int r = 0; r < NSW; ++r) {
-      const int j = wv + 4 * r;
+      const int j = wv + kOrdWaves * r;
       const int l = j < NL ? j : j < 2 * NL ? j - NL : j - 2 * NL;
       bool live = j < NS;
       if (j >= 2 * NL) live = live && a.replace && l >= 1;
@@ -441,7 +442,7 @@ __global__ void __launch_bounds__(256) order_kernel(OrdArgs a) {
     }
 #pragma unroll
     for (int r = 0; r < NSW; ++r) {
-      const int j = wv + 4 * r;
+      const int j = wv + kOrdWaves * r;
       if (lane == 0 && j < NS) bnd[j] = slo[r];
     }
   }
@@ -481,12 +482,13 @@ __global__ void __launch_bounds__(256) order_kernel(OrdArgs a) {
     }
   }
   __syncthreads();
-  // exclusive scan of the flags by words: thread tid owns words [tid CW, tid CW + CW)
-  constexpr int CW = NW / 256;
-  static_assert(NW % 256 == 0 && NF <= 65536, "words split evenly over 256 threads; ranks fit 16 bits");
+  // exclusive scan of the flags by words: thread tid owns words [tid CW, tid CW + CW) of the NW
+  constexpr int CW = (NW + kOrdThreads - 1) / kOrdThreads;
+  static_assert(NF <= 65536, "ranks within a range fit 16 bits");
   int run = 0;
 #pragma unroll
-  for (int x = 0; x < CW; ++x) run += (int)__builtin_popcount(fl[tid * CW + x]);
+  for (int x = 0; x < CW; ++x)
+    if (tid * CW + x < NW) run += (int)__builtin_popcount(fl[tid * CW + x]);
   int inc = run;  // inclusive scan over the wave
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
@@ -499,6 +501,7 @@ __global__ void __launch_bounds__(256) order_kernel(OrdArgs a) {
   for (int w = 0; w < wv; ++w) base += wsum[w];
 #pragma unroll
   for (int x = 0; x < CW; ++x) {
+    if (tid * CW + x >= NW) break;
     wpre[tid * CW + x] = (uint16_t)base;
     base += (int)__builtin_popcount(fl[tid * CW + x]);
   }
@@ -595,14 +598,14 @@ hipError_t lh_launch_select(const LhShape& s, const float* s_qk, const float* s_
   }
   dim3 grid((unsigned)((s.N + kOrdE - 1) / kOrdE), (unsigned)BH);
   switch (s.L) {
-    case 1: hipLaunchKernelGGL(order_kernel<1>, grid, dim3(256), 0, st, o); break;
-    case 2: hipLaunchKernelGGL(order_kernel<2>, grid, dim3(256), 0, st, o); break;
-    case 3: hipLaunchKernelGGL(order_kernel<3>, grid, dim3(256), 0, st, o); break;
-    case 4: hipLaunchKernelGGL(order_kernel<4>, grid, dim3(256), 0, st, o); break;
-    case 5: hipLaunchKernelGGL(order_kernel<5>, grid, dim3(256), 0, st, o); break;
-    case 6: hipLaunchKernelGGL(order_kernel<6>, grid, dim3(256), 0, st, o); break;
-    case 7: hipLaunchKernelGGL(order_kernel<7>, grid, dim3(256), 0, st, o); break;
-    case 8: hipLaunchKernelGGL(order_kernel<8>, grid, dim3(256), 0, st, o); break;
+    case 1: hipLaunchKernelGGL(order_kernel<1>, grid, dim3(kOrdThreads), 0, st, o); break;
+    case 2: hipLaunchKernelGGL(order_kernel<2>, grid, dim3(kOrdThreads), 0, st, o); break;
+    case 3: hipLaunchKernelGGL(order_kernel<3>, grid, dim3(kOrdThreads), 0, st, o); break;
+    case 4: hipLaunchKernelGGL(order_kernel<4>, grid, dim3(kOrdThreads), 0, st, o); break;
+    case 5: hipLaunchKernelGGL(order_kernel<5>, grid, dim3(kOrdThreads), 0, st, o); break;
+    case 6: hipLaunchKernelGGL(order_kernel<6>, grid, dim3(kOrdThreads), 0, st, o); break;
+    case 7: hipLaunchKernelGGL(order_kernel<7>, grid, dim3(kOrdThreads), 0, st, o); break;
+    case 8: hipLaunchKernelGGL(order_kernel<8>, grid, dim3(kOrdThreads), 0, st, o); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

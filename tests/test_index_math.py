@@ -410,6 +410,13 @@ def test_selection_workspace_math(name, c, flags):
         blk = np.repeat(np.arange(gx), hi - lo)
         x = ((ids + 1) * s.pw[l] - 1 - e0[blk]) * s.L + (s.L - 1 - l)
         inside(f"order flag index l{l}", x, x + 1, E * s.L)
+    # the flag scan: 512 threads, thread t owns words [t CW, t CW + CW) clipped to the range's
+    # 8192 L / 32 words, so every word is scanned exactly once and ranks fit 16 bits
+    NW = E * s.L // 32
+    CW = -(-NW // 512)
+    own = np.concatenate([np.arange(t * CW, min(t * CW + CW, NW)) for t in range(512)])
+    once("order scan words", own, NW)
+    assert E * s.L <= 65536
     # every emitted entry gets a distinct rank in [0, S)
     assert s.S <= s.Scand
 
