@@ -704,15 +704,30 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
 
   const int qstart = (k0 / CQ) * CQ;
   const int nqt = (S - qstart + CQ - 1) / CQ;
-  auto stage = [&](auto bufc, int qt0) __attribute__((always_inline)) {
+  // lse and Delta of a query tile enter LDS through the first CQ threads. The tile staged
+  // before the loop is written at once; a tile staged inside the loop has its two values loaded
+  // into nl, nd when its Q / dO copies are issued and written to LDS just before the barrier that
+  // publishes the tile, so no wave waits for those loads in the middle of a tile.
+  float nl = 0.0f, nd = 0.0f;
+  auto put_ld = [&](auto bufc, int qt0, float lv, float dv) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value;
+    const bool in = qt0 + tid < S;
+    (BUF ? ls1 : ls0)[tid] = in ? lv * kLog2e : INFINITY;  // rows past S: P = 0
+    (BUF ? ds1 : ds0)[tid] = in ? -dv : 0.0f;  // negated: it seeds the dP accumulator
+  };
+  auto stage = [&](auto bufc, auto deferc, int qt0) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value;
     if constexpr (IDX) load_tile_idx<D, CQ, KWV, LH_SWZ_K>(BUF ? Qs1 : Qs0, qsrc, q_ids, w, lane);
     else load_tile<D, CQ, KWV, LH_SWZ_K>(BUF ? Qs1 : Qs0, Qh, qt0, S, w, lane);
     load_tile<D, CQ, KWV, LH_SWZ_K>(BUF ? dOs1 : dOs0, dOh, qt0, S, w, lane);
     if (tid < CQ) {
-      const int q = qt0 + tid;
-      (BUF ? ls1 : ls0)[tid] = q < S ? Lh[q] * kLog2e : INFINITY;  // rows past S: P = 0
-      (BUF ? ds1 : ds0)[tid] = q < S ? -Dh[q] : 0.0f;  // negated: it seeds the dP accumulator
+      const int q = qt0 + tid < S ? qt0 + tid : S - 1;  // clamped; rows past S are masked in put_ld
+      if constexpr (decltype(deferc)::value) {
+        nl = Lh[q];
+        nd = Dh[q];
+      } else {
+        put_ld(bufc, qt0, Lh[q], Dh[q]);
+      }
     }
     // tiles are staged from the last one down: the next one starts CQ rows earlier
     if constexpr (IDX) tile_ids<D, CQ, KWV>(idxh, qt0 - CQ > 0 ? qt0 - CQ : 0, S, w, lane, q_ids);
@@ -729,7 +744,7 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
   } else {
     load_tile<D, CK, KWV, LH_SWZ_K>(Kw, Kh, k0, S, w, lane);
   }
-  stage(IC<0>{}, qlast);
+  stage(IC<0>{}, IC<0>{}, qlast);
 
   const int krow = mykey < S ? mykey : S - 1;
   const bf16_t* vrow = IDX ? rs_row(vsrc, idxh[krow]) : Vh + (int64_t)krow * D;
@@ -748,8 +763,9 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
     const float* lt = BUF ? ls1 : ls0;
     const float* dt = BUF ? ds1 : ds0;
     const int qt0 = qlast - it * CQ;
+    if (it > 0 && tid < CQ) put_ld(bufc, qt0, nl, nd);  // staged with the previous tile
     sync_tiles<0>();  // this tile (and its lse / Delta) landed; the other slot is free
-    if (it + 1 < nqt) stage(IC<BUF ^ 1>{}, qt0 - CQ);
+    if (it + 1 < nqt) stage(IC<BUF ^ 1>{}, IC<1>{}, qt0 - CQ);
     if (qt0 + CQ - 1 < kw || kw >= S) return;  // every query of the tile precedes this wave's keys
 #pragma unroll
     for (int qb = 0; qb < CQ / 32; ++qb) {
@@ -820,7 +836,7 @@ sdpa_bwd_dkdv_bf16(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, c
       qsrc = row_src(ix.q, ix.qp, bsb, hs0 * hm.Gq + mq, ix.Hq, ix, D);
       tile_ids<D, CQ, KWV>(idxh, qlast, S, w, lane, q_ids);
     }
-    stage(IC<0>{}, qlast);
+    stage(IC<0>{}, IC<0>{}, qlast);
   }
   // C layout: row = key kw + 8(i/4) + 4h + i%4, column 32 d + lane % 32
 #pragma unroll
