@@ -84,7 +84,8 @@ __device__ __forceinline__ void load_chunk<bf16_t>(const bf16_t* p, float* out) 
 
 // 16-byte store with the non-temporal hint (global_store_dwordx4 ... nt). The streaming
 // kernels write each output chunk once and never read it back, so the lines need not be kept
-// in the caches; measured at c4, the hint takes 3% off the memory stages (the gather 9%).
+// in the caches; measured on the layer at N = 262,144 with 32 query heads, the hint takes 3%
+// off the memory stages (the gather 9%).
 typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void store16_nt(void* p, const u32x4& o) {
   const u32x4v x = {o.x, o.y, o.z, o.w};
